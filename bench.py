@@ -1,0 +1,214 @@
+"""Benchmark of the mixed-state denoising step on one MI355X.
+
+One step = gather (token ids, mask bits) -> dual-cache block attention (every
+layer) -> parallel decode -> scatter (token ids, mask bits), all through
+libblockserve's C ABI on one stream; the block-boundary churn workload (5)
+adds the KV compaction first. Inputs are synthetic and resident in HBM before
+timing. Between steps (outside the per-step events) the decoded token/mask
+state is restored from pristine copies and a 512 MiB buffer is overwritten so
+the 256 MB Infinity Cache holds none of the step's data (cold numbers).
+
+Prints ONE JSON line (rank 0): positions/s, ms per step, per-kernel event
+times, algorithmic HBM traffic, the roofline of the dominant kernel and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def algorithmic_bytes(w):
+    """Bytes the step must move (padding and unmasked rows never counted)."""
+    eb = w.elem
+    lens = (w.reqs["p"] + w.reqs["g"]).astype(np.int64)
+    spans = w.spans()
+    B = np.array([s[1] for s in spans], np.int64)
+    kv = int(lens.sum()) * w.Hkv * w.D * 2 * eb
+    qo = 2 * int(B.sum()) * w.Hq * w.D * eb
+    wt = int(B.sum()) * w.Hkv * w.D * 2 * eb
+    attn = (kv + qo + wt) * w.layers
+    flops = int((4 * B * lens).sum()) * w.Hq * w.D * w.layers
+    return dict(attn=attn, attn_per_layer=attn // w.layers, kv=kv * w.layers, qo=qo * w.layers,
+                write_through=wt * w.layers, attn_flops=flops, positions=int(B.sum()))
+
+
+def build_state(w, dev_logits_fill=True):
+    import torch
+    import synth
+    from paper_2607_08930_amd import step as bstep
+    tok, msk, blk = synth.gen_state(w)
+    layers, host = [], []
+    for l in range(w.layers):
+        q = synth.gen_q(w, l)
+        kn, vn = synth.gen_kv_new(w, l)
+        kc, vc = synth.gen_cache(w, l)
+        out = torch.empty(q.shape, dtype=bstep.torch_dtype(w.dtype), device="cuda")
+        layers.append(bstep.Layer(bstep.to_device(q, w.dtype), bstep.to_device(kn, w.dtype),
+                                  bstep.to_device(vn, w.dtype), bstep.to_device(kc, w.dtype),
+                                  bstep.to_device(vc, w.dtype), out))
+        host.append(dict(q=q, k_new=kn, v_new=vn, k_cache=kc, v_cache=vc))
+    logits = synth.gen_logits(w, blk)
+    st = bstep.StepState(w.L, w.Hq, w.Hkv, w.D, w.V, w.dtype, w.R, w.W, bstep.to_device(tok),
+                         bstep.to_device(msk), layers, bstep.to_device(logits, w.dtype), w.n, tau=w.tau,
+                         q_min=w.q_min, eos_id=w.eos_id).alloc()
+    return st, dict(tokens=tok, mask=msk, blk=blk, layers=host, logits=logits)
+
+
+def masked_rows(blk):
+    return int(blk.sum())
+
+
+def cpu_baseline(w, host, budget_s=12.0):
+    """The oracle as it stands, timed on this host on the same inputs."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    positions = sum(s[1] for s in w.spans())
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
+                                tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 3:
+            break
+    return {"value": positions * reps / el, "unit": "positions/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps} full oracle step(s) of the same workload ({positions} positions, "
+                      f"{w.layers} layer(s)), fp64 NumPy, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload 1-4 (2 = LLaDA-8B-shaped layer)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+    from paper_2607_08930_amd import step as bstep
+
+    assert torch.cuda.is_available()
+    torch.cuda.set_device(0)
+    w = synth.workload(args.config)
+    print(f"[bench] building inputs for {w.name}", file=sys.stderr, flush=True)
+    st, host = build_state(w)
+    ab = algorithmic_bytes(w)
+    nmask = masked_rows(host["blk"])
+    logits_bytes = nmask * w.V * w.elem
+    small_bytes = ab["positions"] * (5 + 5 + 4 + 5 + 5)
+    step_bytes = ab["attn"] + logits_bytes + small_bytes
+    tok0, msk0 = st.tokens.clone(), st.mask.clone()
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    ctx = bs.Context(0)
+
+    names = ["gather", "attention", "decode", "scatter"]
+
+    def one_step(evs=None):
+        L, R, W = st.L, st.R, st.W
+        dt = bstep.dt_code(st.dtype)
+        if evs: evs[0].record(stream)
+        bs.bs_gather_active_blocks(ctx, w.reqs, L, R, W, st.tokens, W * 4, 4, st.tok_c, st.pos)
+        bs.bs_gather_active_blocks(ctx, w.reqs, L, R, W, st.mask, W, 1, st.msk_c, None)
+        if evs: evs[1].record(stream)
+        for lay in st.layers:
+            bs.bs_dual_cache_block_attention(ctx, w.reqs, L, st.Hq, st.Hkv, st.D, dt, 0.0, lay.q, lay.k_new,
+                                             lay.v_new, lay.k_cache, lay.v_cache, R, W, 1, lay.out)
+        if evs: evs[2].record(stream)
+        bs.bs_parallel_decode(ctx, w.reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c,
+                              st.tau, st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, None,
+                              st.dec_ws, st.dec_ws.numel())
+        if evs: evs[3].record(stream)
+        bs.bs_scatter_active_blocks(ctx, w.reqs, L, R, W, st.tok_c, 4, st.tokens, W * 4)
+        bs.bs_scatter_active_blocks(ctx, w.reqs, L, R, W, st.msk_c, 1, st.mask, W)
+        if evs: evs[4].record(stream)
+
+    def reset():
+        st.tokens.copy_(tok0)
+        st.mask.copy_(msk0)
+        if not args.warm:
+            flush.zero_()
+
+    for _ in range(args.warmup):
+        reset()
+        one_step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps); timing {args.steps}", file=sys.stderr, flush=True)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        reset()
+        one_step(evs[k])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / args.steps * 1e3
+    per = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(4)] for k in range(args.steps)])
+    step_ms = per.sum(axis=1)
+    ms = float(np.median(step_ms))
+    attn_ms = float(np.median(per[:, 1])) / w.layers
+    dec_ms = float(np.median(per[:, 2]))
+    value = ab["positions"] / (ms / 1e3)
+    attn_gbs = ab["attn_per_layer"] / (attn_ms / 1e3) / 1e9
+    dec_gbs = logits_bytes / (dec_ms / 1e3) / 1e9
+    attn_dominant = ab["attn"] >= logits_bytes
+    if attn_dominant:
+        roof = {"kernel": "k_attn_bf16" if w.dtype == "bf16" else "k_attn_f32", "bound": "hbm",
+                "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": ab["attn_per_layer"], "avg_launch_ms": round(attn_ms, 5)}
+    else:
+        roof = {"kernel": "k_decode_rows", "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": logits_bytes, "avg_launch_ms": round(dec_ms, 5)}
+    ctx.close()
+    res = {
+        "metric": "denoised block positions/s per mixed-state step",
+        "value": round(value, 1), "unit": "positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "n_requests": w.n, "positions_per_step": ab["positions"],
+                   "masked_rows": nmask, "L": w.L, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "V": w.V,
+                   "layers": w.layers, "sum_len": int((w.reqs["p"] + w.reqs["g"]).sum()),
+                   "cache": "warm" if args.warm else "cold (512 MiB flush between steps)"},
+        "hbm": {"algorithmic_bytes_per_step": step_bytes, "achieved_GBps": round(step_bytes / (ms / 1e3) / 1e9, 1),
+                "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "kernels_ms": {n_: round(float(np.median(per[:, i])), 5) for i, n_ in enumerate(names)},
+        "kernel_GBps": {"attention": round(attn_gbs, 1), "decode": round(dec_gbs, 1)},
+        "attention_tflops": round(ab["attn_flops"] / w.layers / (attn_ms / 1e3) / 1e12, 2),
+        "wall_ms_per_step_incl_restore": round(wall, 5),
+        "step_ms_p10_p90": [round(float(np.percentile(step_ms, 10)), 5), round(float(np.percentile(step_ms, 90)), 5)],
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on the same inputs", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, host)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,218 @@
+/*
+ * blockserve.h -- C ABI of the MI355X (gfx950) mixed-state denoising step.
+ *
+ * One step of BlockServe's block-grained continuous batching (Zhu et al.,
+ * "BlockServe: Block-Grained Continuous Batching for High-Throughput Diffusion
+ * LLM Serving"): every request of a heterogeneous batch sits at its own block
+ * index; the step gathers each request's active block, attends it against the
+ * request's dual KV cache, decodes it with confidence-threshold parallel
+ * decoding, and scatters the result back. At block boundaries the dense KV box
+ * is rewritten when requests are evicted and admitted.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Request descriptor (Section "Problem formulation"): a request has prompt
+ * length p, generation length g, block length L and current block index k
+ * (the paper's b_i), 0 <= k < K = ceil(g / L). Block k covers logical
+ * positions [s, s + B) with s = p + k L and B = min(L, g - k L); the request's
+ * logical row [0, p + g) holds prompt, generated blocks and the still-masked
+ * suffix. Logical position t lives at column off + t of row `row` of every
+ * dense [R][W] tensor (paragraph "Logical positional alignment": left padding,
+ * position ids counted from the first non-padding cell).
+ * A descriptor array is valid when L >= 1 and, for each entry, p >= 0, g >= 1,
+ * 0 <= k < K, 0 <= row < R, off >= 0, off + p + g <= W, and no two entries
+ * share a row.
+ *
+ * Memory: every tensor argument is a DEVICE pointer owned by the caller (this
+ * library allocates no tensor memory). Descriptor and segment arrays are HOST
+ * pointers, read during the call only. Tensors are dense, row-major, in the
+ * layouts stated per call; bf16 is the IEEE upper half of fp32, stored as
+ * 16-bit words.
+ *
+ * Streams: `stream` is a hipStream_t (NULL = the legacy default stream). Every
+ * call only enqueues work on it and never waits for the device; results are
+ * valid after the stream (or an event recorded on it) has completed. Device
+ * pointers must stay valid until then.
+ *
+ * Errors: every int-returning call returns a bs_status. Arguments are checked
+ * on the host BEFORE anything is enqueued, so a failing call launches nothing
+ * and leaves every tensor untouched; bs_last_error() gives the detail.
+ *
+ * Threads: a bs_ctx holds a ring of descriptor upload slots; use one context
+ * per host thread. Calls on one context may target different streams.
+ */
+#ifndef BLOCKSERVE_H
+#define BLOCKSERVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct bs_req_desc {
+  int32_t p;    /* prompt length p_i */
+  int32_t g;    /* generation length g_i */
+  int32_t k;    /* current block index (b_i), 0 <= k < ceil(g / L) */
+  int32_t row;  /* row of the dense box holding this request */
+  int32_t off;  /* column of logical position 0 in that row */
+} bs_req_desc;
+
+typedef struct bs_copy_seg {
+  int32_t src_kind; /* 0: old cache box, 1: staging box */
+  int32_t src_row;
+  int32_t src_col;
+  int32_t dst_row;
+  int32_t dst_col;
+  int32_t len;      /* cached positions to copy (>= 0) */
+} bs_copy_seg;
+
+typedef enum bs_dtype { BS_F32 = 0, BS_BF16 = 1 } bs_dtype;
+
+typedef enum bs_status {
+  BS_OK = 0,
+  BS_ERR_INVALID_ARG = 1,  /* null pointer, bad enum, negative size, bad stride */
+  BS_ERR_UNSUPPORTED = 2,  /* shape/dtype combination this build does not serve */
+  BS_ERR_DESCRIPTOR = 3,   /* descriptor array invalid (see conventions above) */
+  BS_ERR_OVERLAP = 4,      /* copy destinations intersect, or a source aliases a destination */
+  BS_ERR_WORKSPACE = 5,    /* workspace missing or smaller than the size query returns */
+  BS_ERR_HIP = 6           /* HIP runtime or launch failure */
+} bs_status;
+
+typedef struct bs_ctx bs_ctx;
+
+/* Create a context bound to HIP device `device` (it becomes current while the
+ * library works). The context owns only pinned host staging memory and device
+ * upload slots for descriptors and work lists. *out is NULL on failure. */
+int bs_create(bs_ctx** out, int device);
+
+/* Wait for every upload slot to drain, then free the context (NULL is OK). */
+int bs_destroy(bs_ctx* ctx);
+
+/* Static text for a status code. */
+const char* bs_status_string(int status);
+
+/* Detail of the last failure on this context ("" if none; ctx may be NULL,
+ * which returns the detail of the last failure of a context-free call). */
+const char* bs_last_error(const bs_ctx* ctx);
+
+/* Host-only check of a descriptor array against block length L and an
+ * R x W box (the rules under "Conventions"). Touches no device. */
+int bs_validate_requests(const bs_req_desc* reqs, int n, int L, int R, int W);
+
+/*
+ * K1 -- gather of the active blocks (paragraph "Vectorized mixed-schedule
+ * execution": gather extracts each request's active block region into a
+ * compact tensor).
+ *   dst[i][j] = src[row_i][off_i + s_i + j]   for j < B_i, else all-zero bytes
+ *   pos_out[i][j] = s_i + j                   for j < B_i, else -1
+ * src: dense [R][W] elements of `elem_bytes` bytes (1, 2, 4, 8 or 16), rows
+ * `src_row_stride_bytes` apart (>= W * elem_bytes). dst: compact [n][L]
+ * elements, contiguous. pos_out: [n][L] int32 or NULL. n == 0 is a no-op.
+ */
+int bs_gather_active_blocks(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W,
+                            const void* src, int64_t src_row_stride_bytes, int elem_bytes,
+                            void* dst, int32_t* pos_out, void* stream);
+
+/* Inverse of K1 (paragraph "Vectorized mixed-schedule execution": scatter
+ * writes results back to the corresponding positions):
+ *   dst[row_i][off_i + s_i + j] = src[i][j]   for j < B_i.
+ * No other cell of dst is written. */
+int bs_scatter_active_blocks(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W,
+                             const void* src_compact, int elem_bytes, void* dst_dense,
+                             int64_t dst_row_stride_bytes, void* stream);
+
+/*
+ * K2 -- dual-cache block attention for one layer (paragraph "Vectorized
+ * mixed-schedule execution": the active block is computed against the cached
+ * KV and the fresh block KV is written in place at the physical offsets of the
+ * request's current block only; dual cache = cached prefix + cached masked
+ * suffix, the Fast-dLLM mechanism the paper integrates, Sections
+ * "Experimental setup" and "Diffusion LLM Inference Optimization").
+ * For request i, query head h (KV head c = h / (Hq / Hkv)) and block row
+ * j < B_i, with keys/values = [cache cols off+[0,s) | k_new/v_new rows [0,B) |
+ * cache cols off+[s+B, p+g)] of row_i, head c:
+ *   out[i][j][h] = softmax(scale * q[i][j][h] . keys^T) . values
+ * (bidirectional, no cross-request or padding keys). out rows j >= B_i are
+ * written as zeros. scale <= 0 selects 1/sqrt(D).
+ * Layouts (element type `dt` for all five tensors):
+ *   q, out        [n][L][Hq][D]      k_new, v_new  [n][L][Hkv][D]
+ *   k_cache, v_cache [R][Hkv][W][D]
+ * write_back != 0 additionally stores k_new/v_new rows j < B_i into the cache
+ * cells [off_i + s_i + j] of head c (no other cache cell is written); with 0
+ * the caches are only read.
+ * Supported: Hq % Hkv == 0; BS_F32 with D % 4 == 0, D <= 256; BS_BF16 with
+ * D in {64, 128}, L <= 64 and (Hq / Hkv) * ceil(L / 32) <= 8. All pointers
+ * 16-byte aligned. Cache cells outside each request's logical row and the
+ * stale block slot are never read (they may hold NaN).
+ * ws: device workspace of at least bs_attention_workspace_bytes(...) bytes
+ * (NULL allowed when that is 0). Its contents need no initialisation.
+ */
+size_t bs_attention_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
+                                    bs_dtype dt);
+int bs_dual_cache_block_attention(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int Hq,
+                                  int Hkv, int D, bs_dtype dt, float scale, const void* q,
+                                  const void* k_new, const void* v_new, void* k_cache,
+                                  void* v_cache, int R, int W, int write_back, void* out,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * K3 -- confidence-aware parallel decode of the active blocks (paragraph
+ * "Vectorized mixed-schedule execution": per-step transfer quota; greedy
+ * decoding, "Implementation details"; Fast-dLLM's threshold rule integrated
+ * unchanged). For request i let M = { j < B_i : masked[i][j] != 0 }. For j in M:
+ *   x_j = argmax_v logits[i][j][v]                (ties: smallest v)
+ *   c_j = 1 / sum_v exp(logits[i][j][v] - max_v)  (max softmax probability)
+ * n_i = min(|M|, max(q_min, #{j in M : c_j >= tau})); the n_i most confident
+ * positions of M (ties: smallest j) get tokens[i][j] = x_j, masked[i][j] = 0.
+ * Every other cell of tokens/masked is left unchanged (no re-masking).
+ * Outputs: n_unmasked[i] = n_i; done[i] = (n_i == |M|); eos_seen[i] = some
+ * j < B_i has masked == 0 and tokens == eos_id after the update (always 0 when
+ * eos_id < 0); conf_out[i][j] = c_j for j in M, -1 otherwise (conf_out may be
+ * NULL). A request with M empty is a no-op with done = 1.
+ * logits: [n][L] rows of V elements of `logits_dt`, row (i, j) starting at
+ * logits + (i * L + j) * logits_row_stride elements (stride >= V, stride *
+ * element size a multiple of 16 bytes, base 16-byte aligned). Only rows
+ * j in M are read; they must be finite. tokens [n][L] int32 and masked [n][L]
+ * uint8 are updated in place. q_min >= 1 (at least one unmask per step while
+ * any position is masked); L <= 64.
+ * ws: device workspace of at least bs_decode_workspace_bytes(...) bytes; its
+ * contents need no initialisation.
+ */
+size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype logits_dt);
+int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V,
+                       bs_dtype logits_dt, const void* logits, int64_t logits_row_stride,
+                       int32_t* tokens, uint8_t* masked, float tau, int32_t q_min, int32_t eos_id,
+                       int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen, float* conf_out,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * K4 -- KV scatter/compaction at a block boundary (Algorithm 1: completed
+ * requests leave and new ones are admitted at the block boundary; Eq. 1
+ * discussion: the box shrinks without explicit reclamation; paragraph
+ * "Vectorized mixed-schedule execution": the frozen prefix cache survives
+ * batch reconfiguration). For every segment, layer l < n_layers, KV head
+ * h < Hkv and t < len, for K and for V:
+ *   dst[l][dst_row][h][dst_col + t] = S[l][src_row][h][src_col + t]
+ * where S is the old box (src_kind 0) or the staging box (src_kind 1).
+ * Boxes are [n_layers][R_x][Hkv][W_x][D] of `dt`, layers `*_layer_stride`
+ * BYTES apart (>= R_x * Hkv * W_x * D * elem). Every other dst cell is left
+ * unchanged. Rules (BS_ERR_OVERLAP otherwise): destination ranges are
+ * pairwise disjoint; when a source box is the destination box (same
+ * pointers), no source range of a segment intersects any destination range.
+ * D * elem must be a multiple of 16 bytes. stg_* may be NULL when no segment
+ * has src_kind 1; src_* may be NULL when none has src_kind 0.
+ */
+int bs_kv_scatter_compact(bs_ctx* ctx, const bs_copy_seg* segs, int nseg, int n_layers, int Hkv,
+                          int D, bs_dtype dt, const void* src_k, const void* src_v,
+                          int64_t src_layer_stride, int R_src, int W_src, const void* stg_k,
+                          const void* stg_v, int64_t stg_layer_stride, int R_stg, int W_stg,
+                          void* dst_k, void* dst_v, int64_t dst_layer_stride, int R_dst, int W_dst,
+                          void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BLOCKSERVE_H */

@@ -1,0 +1,231 @@
+"""Python binding of libblockserve.so, the MI355X (gfx950) mixed-state
+denoising step of BlockServe (block-grained continuous batching for diffusion
+LLMs).
+
+Argument marshalling only: every entry point forwards to the C ABI declared in
+``include/blockserve.h`` under the same name; all work happens in the HIP
+kernels of the library. Tensors are passed as torch device tensors (or raw
+integer device addresses); descriptor and segment arrays as numpy structured
+arrays with the C struct layouts ``REQ_DTYPE`` / ``SEG_DTYPE``. A nonzero
+status raises ``BlockServeError``. There is no CPU implementation: importing
+this package fails when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = [
+    "REQ_DTYPE", "SEG_DTYPE", "BS_F32", "BS_BF16", "BlockServeError", "Context", "lib", "LIB_PATH",
+    "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
+    "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_attention_workspace_bytes",
+    "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
+    "bs_kv_scatter_compact",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libblockserve.so")
+
+REQ_DTYPE = np.dtype([("p", "<i4"), ("g", "<i4"), ("k", "<i4"), ("row", "<i4"), ("off", "<i4")])
+SEG_DTYPE = np.dtype([("src_kind", "<i4"), ("src_row", "<i4"), ("src_col", "<i4"),
+                      ("dst_row", "<i4"), ("dst_col", "<i4"), ("len", "<i4")])
+BS_F32, BS_BF16 = 0, 1
+STATUS = {0: "BS_OK", 1: "BS_ERR_INVALID_ARG", 2: "BS_ERR_UNSUPPORTED", 3: "BS_ERR_DESCRIPTOR",
+          4: "BS_ERR_OVERLAP", 5: "BS_ERR_WORKSPACE", 6: "BS_ERR_HIP"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2607_08930_amd.build)")
+
+# PyTorch-ROCm ships its own libamdhip64.so with the same soname as ROCm's.
+# Loading torch first makes the dynamic linker bind this library to torch's
+# HIP runtime, so torch's streams, events and allocations are the ones the
+# kernels see; two runtimes in one process would not share them.
+import torch  # noqa: E402,F401
+
+
+def _hip_runtimes() -> set:
+    found = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                p = line.split()[-1] if line.strip() else ""
+                if "libamdhip64" in p:
+                    found.add(os.path.realpath(p))
+    except OSError:
+        pass
+    return found
+
+
+lib = ctypes.CDLL(LIB_PATH)
+if len(_hip_runtimes()) > 1:
+    raise ImportError("two HIP runtimes are loaded in this process (" + ", ".join(sorted(_hip_runtimes()))
+                      + "): import torch before loading libblockserve.so")
+
+_vp, _i32, _i64, _f32, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+_SIGS = {
+    "bs_create": (_i32, [ctypes.POINTER(_vp), _i32]),
+    "bs_destroy": (_i32, [_vp]),
+    "bs_status_string": (ctypes.c_char_p, [_i32]),
+    "bs_last_error": (ctypes.c_char_p, [_vp]),
+    "bs_validate_requests": (_i32, [_vp, _i32, _i32, _i32, _i32]),
+    "bs_gather_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _i32, _vp, _vp, _vp]),
+    "bs_scatter_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i64, _vp]),
+    "bs_attention_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
+    "bs_dual_cache_block_attention": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
+                                             _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
+    "bs_decode_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32]),
+    "bs_parallel_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _f32, _i32, _i32,
+                                  _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bs_kv_scatter_compact": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp,
+                                     _vp, _i64, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+class BlockServeError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+        super().__init__(f"{self.name}: {detail}")
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if isinstance(x, Context):
+        return x.handle
+    raise TypeError(f"cannot pass {type(x)} as a pointer")
+
+
+def _host(arr, dtype):
+    a = np.ascontiguousarray(arr)
+    if a.dtype != dtype:
+        a = a.astype(dtype)
+    return a
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(st: int, ctx=None):
+    if st != 0:
+        detail = lib.bs_last_error(_ptr(ctx) if ctx is not None else None)
+        raise BlockServeError(st, detail.decode() if detail else "")
+    return st
+
+
+class Context:
+    """Owns a bs_ctx (upload ring for descriptors); close() or use as a context manager."""
+
+    def __init__(self, device: int = 0):
+        h = _vp()
+        _check(lib.bs_create(ctypes.byref(h), device))
+        self.handle = h.value
+        self.device = device
+
+    def close(self):
+        if self.handle:
+            lib.bs_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def bs_create(device: int = 0) -> Context:
+    return Context(device)
+
+
+def bs_destroy(ctx: Context) -> None:
+    ctx.close()
+
+
+def bs_status_string(status: int) -> str:
+    return lib.bs_status_string(status).decode()
+
+
+def bs_last_error(ctx: Context | None = None) -> str:
+    return lib.bs_last_error(_ptr(ctx) if ctx is not None else None).decode()
+
+
+def bs_validate_requests(reqs, L: int, R: int, W: int) -> None:
+    r = _host(reqs, REQ_DTYPE)
+    _check(lib.bs_validate_requests(_ptr(r), len(r), L, R, W))
+
+
+def bs_gather_active_blocks(ctx, reqs, L, R, W, src, src_row_stride_bytes, elem_bytes, dst, pos_out=None,
+                            stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    return _check(lib.bs_gather_active_blocks(_ptr(ctx), _ptr(r), len(r), L, R, W, _ptr(src),
+                                              src_row_stride_bytes, elem_bytes, _ptr(dst), _ptr(pos_out),
+                                              _stream(stream)), ctx)
+
+
+def bs_scatter_active_blocks(ctx, reqs, L, R, W, src_compact, elem_bytes, dst_dense, dst_row_stride_bytes,
+                             stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    return _check(lib.bs_scatter_active_blocks(_ptr(ctx), _ptr(r), len(r), L, R, W, _ptr(src_compact),
+                                               elem_bytes, _ptr(dst_dense), dst_row_stride_bytes,
+                                               _stream(stream)), ctx)
+
+
+def bs_attention_workspace_bytes(reqs, L, Hq, Hkv, D, dt) -> int:
+    r = _host(reqs, REQ_DTYPE)
+    return int(lib.bs_attention_workspace_bytes(_ptr(r), len(r), L, Hq, Hkv, D, dt))
+
+
+def bs_dual_cache_block_attention(ctx, reqs, L, Hq, Hkv, D, dt, scale, q, k_new, v_new, k_cache, v_cache, R,
+                                  W, write_back, out, ws=None, ws_bytes=0, stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    return _check(lib.bs_dual_cache_block_attention(
+        _ptr(ctx), _ptr(r), len(r), L, Hq, Hkv, D, dt, float(scale), _ptr(q), _ptr(k_new), _ptr(v_new),
+        _ptr(k_cache), _ptr(v_cache), R, W, int(write_back), _ptr(out), _ptr(ws), int(ws_bytes),
+        _stream(stream)), ctx)
+
+
+def bs_decode_workspace_bytes(n, L, V, dt) -> int:
+    return int(lib.bs_decode_workspace_bytes(n, L, V, dt))
+
+
+def bs_parallel_decode(ctx, reqs, L, V, logits_dt, logits, logits_row_stride, tokens, masked, tau, q_min,
+                       eos_id, n_unmasked, done, eos_seen, conf_out=None, ws=None, ws_bytes=0, stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    return _check(lib.bs_parallel_decode(
+        _ptr(ctx), _ptr(r), len(r), L, V, logits_dt, _ptr(logits), int(logits_row_stride), _ptr(tokens),
+        _ptr(masked), float(tau), int(q_min), int(eos_id), _ptr(n_unmasked), _ptr(done), _ptr(eos_seen),
+        _ptr(conf_out), _ptr(ws), int(ws_bytes), _stream(stream)), ctx)
+
+
+def bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt, src_k, src_v, src_layer_stride, R_src, W_src,
+                          stg_k, stg_v, stg_layer_stride, R_stg, W_stg, dst_k, dst_v, dst_layer_stride,
+                          R_dst, W_dst, stream=None):
+    s = _host(segs, SEG_DTYPE)
+    return _check(lib.bs_kv_scatter_compact(
+        _ptr(ctx), _ptr(s), len(s), n_layers, Hkv, D, dt, _ptr(src_k), _ptr(src_v), int(src_layer_stride),
+        R_src, W_src, _ptr(stg_k), _ptr(stg_v), int(stg_layer_stride), R_stg, W_stg, _ptr(dst_k),
+        _ptr(dst_v), int(dst_layer_stride), R_dst, W_dst, _stream(stream)), ctx)

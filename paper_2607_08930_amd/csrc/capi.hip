@@ -1,0 +1,491 @@
+// Host side of the C ABI declared in include/blockserve.h: argument and
+// descriptor validation (before anything is enqueued), work-list construction,
+// descriptor upload through a content-addressed ring of pinned/device slots,
+// and kernel launches on the caller's stream.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "bs_internal.h"
+
+using namespace bs;
+
+namespace {
+
+constexpr int kSlots = 16;
+
+struct Slot {
+  void* d = nullptr;       // device copy
+  void* h = nullptr;       // pinned staging copy (immutable while live)
+  size_t cap = 0;
+  size_t nbytes = 0;
+  uint64_t hash = 0;
+  hipEvent_t ready = nullptr;  // recorded after the upload
+  hipEvent_t done = nullptr;   // recorded after the last launch that read it
+  hipStream_t stream = nullptr;
+  bool live = false;
+};
+
+thread_local std::string g_err;
+
+uint64_t fnv1a(const void* p, size_t n) {
+  const unsigned char* b = static_cast<const unsigned char*>(p);
+  uint64_t h = 1469598103934665603ull;
+  for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+  return h ^ n;
+}
+
+}  // namespace
+
+struct bs_ctx {
+  int device = 0;
+  Slot slots[kSlots];
+  int next = 0;
+  std::string err;
+};
+
+namespace {
+
+int fail(bs_ctx* c, int st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c)
+    c->err = buf;
+  else
+    g_err = buf;
+  return st;
+}
+
+int hip_fail(bs_ctx* c, hipError_t e, const char* what) {
+  return fail(c, BS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Makes the context's device current for the duration of a call.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+int check_reqs(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W) {
+  if (n < 0) return fail(c, BS_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !reqs) return fail(c, BS_ERR_INVALID_ARG, "reqs is NULL");
+  if (L < 1) return fail(c, BS_ERR_DESCRIPTOR, "L < 1");
+  if (R < 1 || W < 1) return fail(c, BS_ERR_INVALID_ARG, "box R=%d W=%d must be >= 1", R, W);
+  std::vector<unsigned char> seen((size_t)R, 0);
+  for (int i = 0; i < n; ++i) {
+    const bs_req_desc& r = reqs[i];
+    if (r.p < 0 || r.g < 1) return fail(c, BS_ERR_DESCRIPTOR, "request %d: p=%d g=%d (need p >= 0, g >= 1)", i, r.p, r.g);
+    const int64_t K = ((int64_t)r.g + L - 1) / L;
+    if (r.k < 0 || r.k >= K) return fail(c, BS_ERR_DESCRIPTOR, "request %d: block index %d outside [0, %lld)", i, r.k, (long long)K);
+    if (r.row < 0 || r.row >= R) return fail(c, BS_ERR_DESCRIPTOR, "request %d: row %d outside [0, %d)", i, r.row, R);
+    if (seen[r.row]) return fail(c, BS_ERR_DESCRIPTOR, "request %d: row %d used twice", i, r.row);
+    seen[r.row] = 1;
+    if (r.off < 0 || (int64_t)r.off + r.p + r.g > W)
+      return fail(c, BS_ERR_DESCRIPTOR, "request %d: off=%d + p+g=%d exceeds W=%d", i, r.off, r.p + r.g, W);
+  }
+  return BS_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Upload `n` bytes of host data; reuses a live slot with identical contents.
+int upload(bs_ctx* c, hipStream_t s, const void* data, size_t n, Slot** out) {
+  const uint64_t hv = fnv1a(data, n);
+  for (Slot& sl : c->slots) {
+    if (sl.live && sl.hash == hv && sl.nbytes == n && std::memcmp(sl.h, data, n) == 0) {
+      if (sl.stream != s) {
+        hipError_t e = hipStreamWaitEvent(s, sl.done, 0);
+        if (e != hipSuccess) return hip_fail(c, e, "hipStreamWaitEvent");
+        sl.stream = s;
+      }
+      *out = &sl;
+      return BS_OK;
+    }
+  }
+  Slot& sl = c->slots[c->next];
+  c->next = (c->next + 1) % kSlots;
+  if (sl.live) {
+    hipError_t e = hipEventSynchronize(sl.done);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize(slot)");
+    sl.live = false;
+  }
+  if (sl.cap < n) {
+    if (sl.d) (void)hipFree(sl.d);
+    if (sl.h) (void)hipHostFree(sl.h);
+    sl.d = sl.h = nullptr;
+    sl.cap = 0;
+    size_t cap = 65536;
+    while (cap < n) cap *= 2;
+    hipError_t e = hipMalloc(&sl.d, cap);
+    if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(upload slot)");
+    e = hipHostMalloc(&sl.h, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(c, e, "hipHostMalloc(upload slot)");
+    sl.cap = cap;
+  }
+  if (!sl.ready) {
+    hipError_t e = hipEventCreateWithFlags(&sl.ready, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventCreate");
+  }
+  std::memcpy(sl.h, data, n);
+  hipError_t e = hipMemcpyAsync(sl.d, sl.h, n, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync(upload)");
+  e = hipEventRecord(sl.ready, s);
+  if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+  sl.hash = hv;
+  sl.nbytes = n;
+  sl.stream = s;
+  sl.live = true;
+  *out = &sl;
+  return BS_OK;
+}
+
+int finish(bs_ctx* c, Slot* sl, hipStream_t s, hipError_t launch, const char* what) {
+  hipError_t e = hipEventRecord(sl->done, s);
+  if (launch != hipSuccess) return hip_fail(c, launch, what);
+  if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord(done)");
+  return BS_OK;
+}
+
+// Blob = descriptors followed by an optional work list, 16-byte aligned parts.
+struct Blob {
+  std::vector<unsigned char> bytes;
+  size_t add(const void* p, size_t n) {
+    size_t off = (bytes.size() + 15) & ~size_t(15);
+    bytes.resize(off + n);
+    if (n) std::memcpy(bytes.data() + off, p, n);
+    return off;
+  }
+};
+
+int dtype_bytes(bs_dtype dt) { return dt == BS_F32 ? 4 : (dt == BS_BF16 ? 2 : 0); }
+
+}  // namespace
+
+extern "C" {
+
+int bs_create(bs_ctx** out, int device) {
+  if (!out) return fail(nullptr, BS_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int count = 0;
+  hipError_t e = hipGetDeviceCount(&count);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "hipGetDeviceCount");
+  if (device < 0 || device >= count) return fail(nullptr, BS_ERR_INVALID_ARG, "device %d of %d", device, count);
+  bs_ctx* c = new bs_ctx();
+  c->device = device;
+  *out = c;
+  return BS_OK;
+}
+
+int bs_destroy(bs_ctx* c) {
+  if (!c) return BS_OK;
+  DeviceGuard dg(c->device);
+  for (Slot& sl : c->slots) {
+    if (sl.live) (void)hipEventSynchronize(sl.done);
+    if (sl.d) (void)hipFree(sl.d);
+    if (sl.h) (void)hipHostFree(sl.h);
+    if (sl.ready) (void)hipEventDestroy(sl.ready);
+    if (sl.done) (void)hipEventDestroy(sl.done);
+  }
+  delete c;
+  return BS_OK;
+}
+
+const char* bs_status_string(int st) {
+  switch (st) {
+    case BS_OK: return "BS_OK";
+    case BS_ERR_INVALID_ARG: return "BS_ERR_INVALID_ARG";
+    case BS_ERR_UNSUPPORTED: return "BS_ERR_UNSUPPORTED";
+    case BS_ERR_DESCRIPTOR: return "BS_ERR_DESCRIPTOR";
+    case BS_ERR_OVERLAP: return "BS_ERR_OVERLAP";
+    case BS_ERR_WORKSPACE: return "BS_ERR_WORKSPACE";
+    case BS_ERR_HIP: return "BS_ERR_HIP";
+    default: return "BS_UNKNOWN_STATUS";
+  }
+}
+
+const char* bs_last_error(const bs_ctx* c) { return c ? c->err.c_str() : g_err.c_str(); }
+
+int bs_validate_requests(const bs_req_desc* reqs, int n, int L, int R, int W) {
+  return check_reqs(nullptr, reqs, n, L, R, W);
+}
+
+// ------------------------------------------------------------------ K1
+static int gather_common(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
+                         const void* a_ptr, int64_t stride, int eb, void* b_ptr, bool gather,
+                         int32_t* pos, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  int st = check_reqs(c, reqs, n, L, R, W);
+  if (st) return st;
+  if (!(eb == 1 || eb == 2 || eb == 4 || eb == 8 || eb == 16))
+    return fail(c, BS_ERR_UNSUPPORTED, "elem_bytes=%d (supported: 1, 2, 4, 8, 16)", eb);
+  if (n == 0) return BS_OK;
+  if (!a_ptr || !b_ptr) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (stride < (int64_t)W * eb) return fail(c, BS_ERR_INVALID_ARG, "row stride %lld < W*elem", (long long)stride);
+  if (stride % eb || !aligned(a_ptr, eb) || !aligned(b_ptr, eb) || (pos && !aligned(pos, 4)))
+    return fail(c, BS_ERR_INVALID_ARG, "pointers and row stride must be multiples of elem_bytes");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  st = upload(c, s, reqs, sizeof(bs_req_desc) * n, &sl);
+  if (st) return st;
+  const bs_req_desc* dreqs = static_cast<const bs_req_desc*>(sl->d);
+  hipError_t e = gather ? launch_gather(dreqs, n, L, a_ptr, stride, eb, b_ptr, pos, s)
+                        : launch_scatter(dreqs, n, L, a_ptr, eb, b_ptr, stride, s);
+  return finish(c, sl, s, e, gather ? "gather launch" : "scatter launch");
+}
+
+int bs_gather_active_blocks(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
+                            const void* src, int64_t src_row_stride_bytes, int elem_bytes,
+                            void* dst, int32_t* pos_out, void* stream) {
+  return gather_common(c, reqs, n, L, R, W, src, src_row_stride_bytes, elem_bytes, dst, true, pos_out, stream);
+}
+
+int bs_scatter_active_blocks(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
+                             const void* src_compact, int elem_bytes, void* dst_dense,
+                             int64_t dst_row_stride_bytes, void* stream) {
+  return gather_common(c, reqs, n, L, R, W, src_compact, dst_row_stride_bytes, elem_bytes, dst_dense, false,
+                       nullptr, stream);
+}
+
+// ------------------------------------------------------------------ K2
+size_t bs_attention_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
+                                    bs_dtype dt) {
+  (void)reqs; (void)n; (void)L; (void)Hq; (void)Hkv; (void)D; (void)dt;
+  return 0;
+}
+
+int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int Hq,
+                                  int Hkv, int D, bs_dtype dt, float scale, const void* q,
+                                  const void* k_new, const void* v_new, void* k_cache,
+                                  void* v_cache, int R, int W, int write_back, void* out,
+                                  void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  int st = check_reqs(c, reqs, n, L, R, W);
+  if (st) return st;
+  if (dt != BS_F32 && dt != BS_BF16) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)dt);
+  if (Hq < 1 || Hkv < 1 || D < 1) return fail(c, BS_ERR_INVALID_ARG, "Hq, Hkv, D must be >= 1");
+  if (Hq % Hkv) return fail(c, BS_ERR_UNSUPPORTED, "Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
+  const int G = Hq / Hkv, RB = (L + 31) / 32;
+  if (dt == BS_F32 && (D % 4 || D > 256)) return fail(c, BS_ERR_UNSUPPORTED, "fp32 path needs D %% 4 == 0 and D <= 256 (D=%d)", D);
+  if (dt == BS_BF16) {
+    if (D != 64 && D != 128) return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs D in {64, 128} (D=%d)", D);
+    if (L > 64 || G * RB > 8)
+      return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs L <= 64 and (Hq/Hkv)*ceil(L/32) <= 8 (got %d)", G * RB);
+  }
+  const size_t need = bs_attention_workspace_bytes(reqs, n, L, Hq, Hkv, D, dt);
+  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  if (n == 0) return BS_OK;
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !out) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(out, 16))
+    return fail(c, BS_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  Blob blob;
+  const size_t off_reqs = blob.add(reqs, sizeof(bs_req_desc) * n);
+  size_t off_items = 0;
+  int n_items = 0;
+  if (dt == BS_BF16) {
+    std::vector<AttnItem> items;
+    items.reserve((size_t)n * Hkv);
+    for (int i = 0; i < n; ++i) {
+      const int len = reqs[i].p + reqs[i].g;
+      for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, 0, len, 0, 1, 0, 0});
+    }
+    // longest rows first so the tail of the grid is made of short items
+    std::stable_sort(items.begin(), items.end(),
+                     [](const AttnItem& x, const AttnItem& y) { return (x.t1 - x.t0) > (y.t1 - y.t0); });
+    n_items = (int)items.size();
+    off_items = blob.add(items.data(), sizeof(AttnItem) * items.size());
+  }
+  Slot* sl = nullptr;
+  st = upload(c, s, blob.bytes.data(), blob.bytes.size(), &sl);
+  if (st) return st;
+  const char* base = static_cast<const char*>(sl->d);
+  AttnArgs a{};
+  a.reqs = reinterpret_cast<const bs_req_desc*>(base + off_reqs);
+  a.items = reinterpret_cast<const AttnItem*>(base + off_items);
+  a.n_items = n_items;
+  a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = G; a.RB = RB; a.R = R; a.W = W;
+  a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
+  a.scale_log2e = a.scale * 1.4426950408889634f;
+  a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
+  a.write_back = write_back ? 1 : 0;
+  a.ws_o = nullptr; a.ws_ml = nullptr;
+  (void)ws;
+  hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, n, 0, s);
+  return finish(c, sl, s, e, "attention launch");
+}
+
+// ------------------------------------------------------------------ K3
+size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype dt) {
+  const int eb = dtype_bytes(dt);
+  if (n <= 0 || L <= 0 || V <= 0 || eb == 0) return 0;
+  const int64_t per = kDecChunkBytes / eb;
+  const int64_t nchunk = ((int64_t)V + per - 1) / per;
+  return (size_t)n * L * nchunk * sizeof(DecPartial);
+}
+
+int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
+                       bs_dtype logits_dt, const void* logits, int64_t logits_row_stride,
+                       int32_t* tokens, uint8_t* masked, float tau, int32_t q_min, int32_t eos_id,
+                       int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen, float* conf_out,
+                       void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  if (n < 0) return fail(c, BS_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !reqs) return fail(c, BS_ERR_INVALID_ARG, "reqs is NULL");
+  if (L < 1) return fail(c, BS_ERR_DESCRIPTOR, "L < 1");
+  for (int i = 0; i < n; ++i) {
+    const bs_req_desc& r = reqs[i];
+    const int64_t K = ((int64_t)r.g + L - 1) / L;
+    if (r.p < 0 || r.g < 1 || r.k < 0 || r.k >= K)
+      return fail(c, BS_ERR_DESCRIPTOR, "request %d: p=%d g=%d k=%d invalid for L=%d", i, r.p, r.g, r.k, L);
+  }
+  const int eb = dtype_bytes(logits_dt);
+  if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)logits_dt);
+  if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
+  if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
+  if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
+  if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
+  if (logits_row_stride < V || (logits_row_stride * eb) % 16)
+    return fail(c, BS_ERR_INVALID_ARG, "logits row stride %lld must be >= V and a multiple of 16 bytes",
+                (long long)logits_row_stride);
+  const size_t need = bs_decode_workspace_bytes(n, L, V, logits_dt);
+  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  if (n == 0) return BS_OK;
+  if (!logits || !tokens || !masked || !n_unmasked || !done || !eos_seen)
+    return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(logits, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) || !aligned(ws, 16) ||
+      (conf_out && !aligned(conf_out, 4)))
+    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (logits and ws need 16 bytes)");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  int st = upload(c, s, reqs, sizeof(bs_req_desc) * n, &sl);
+  if (st) return st;
+  DecArgs a{};
+  a.reqs = static_cast<const bs_req_desc*>(sl->d);
+  a.n = n; a.L = L; a.V = V;
+  a.nchunk = (int)(((int64_t)V + kDecChunkBytes / eb - 1) / (kDecChunkBytes / eb));
+  a.logits = logits; a.row_stride = logits_row_stride;
+  a.tokens = tokens; a.masked = masked; a.tau = tau; a.q_min = q_min; a.eos_id = eos_id;
+  a.n_unmasked = n_unmasked; a.done = done; a.eos_seen = eos_seen; a.conf_out = conf_out;
+  a.part = static_cast<DecPartial*>(ws);
+  hipError_t e = launch_decode(a, logits_dt, s);
+  return finish(c, sl, s, e, "decode launch");
+}
+
+// ------------------------------------------------------------------ K4
+int bs_kv_scatter_compact(bs_ctx* c, const bs_copy_seg* segs, int nseg, int n_layers, int Hkv,
+                          int D, bs_dtype dt, const void* src_k, const void* src_v,
+                          int64_t src_layer_stride, int R_src, int W_src, const void* stg_k,
+                          const void* stg_v, int64_t stg_layer_stride, int R_stg, int W_stg,
+                          void* dst_k, void* dst_v, int64_t dst_layer_stride, int R_dst, int W_dst,
+                          void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  const int eb = dtype_bytes(dt);
+  if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)dt);
+  if (nseg < 0 || n_layers < 0 || Hkv < 1 || D < 1) return fail(c, BS_ERR_INVALID_ARG, "negative or zero size");
+  if (nseg > 0 && !segs) return fail(c, BS_ERR_INVALID_ARG, "segs is NULL");
+  const int64_t row_bytes = (int64_t)D * eb;
+  if (row_bytes % 16) return fail(c, BS_ERR_UNSUPPORTED, "D*elem=%lld not a multiple of 16 bytes", (long long)row_bytes);
+  bool any_src = false, any_stg = false;
+  int64_t total_chunks = 0;
+  for (int i = 0; i < nseg; ++i) {
+    const bs_copy_seg& g = segs[i];
+    if (g.len < 0) return fail(c, BS_ERR_INVALID_ARG, "segment %d: len < 0", i);
+    if (g.src_kind != 0 && g.src_kind != 1) return fail(c, BS_ERR_INVALID_ARG, "segment %d: src_kind %d", i, g.src_kind);
+    const int Rs = g.src_kind ? R_stg : R_src, Ws = g.src_kind ? W_stg : W_src;
+    if (g.src_kind) any_stg = true; else any_src = true;
+    if (g.src_row < 0 || g.src_row >= Rs || g.src_col < 0 || (int64_t)g.src_col + g.len > Ws)
+      return fail(c, BS_ERR_INVALID_ARG, "segment %d: source range outside its box", i);
+    if (g.dst_row < 0 || g.dst_row >= R_dst || g.dst_col < 0 || (int64_t)g.dst_col + g.len > W_dst)
+      return fail(c, BS_ERR_INVALID_ARG, "segment %d: destination range outside the box", i);
+    total_chunks += (g.len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
+  }
+  if (any_src && (!src_k || !src_v)) return fail(c, BS_ERR_INVALID_ARG, "src box is NULL");
+  if (any_stg && (!stg_k || !stg_v)) return fail(c, BS_ERR_INVALID_ARG, "staging box is NULL");
+  if (nseg > 0 && (!dst_k || !dst_v)) return fail(c, BS_ERR_INVALID_ARG, "dst box is NULL");
+  auto box_ok = [&](int64_t ls, int Rb, int Wb) { return ls >= (int64_t)Rb * Hkv * Wb * row_bytes && ls % 16 == 0; };
+  if ((any_src && !box_ok(src_layer_stride, R_src, W_src)) || (any_stg && !box_ok(stg_layer_stride, R_stg, W_stg)) ||
+      (nseg > 0 && !box_ok(dst_layer_stride, R_dst, W_dst)))
+    return fail(c, BS_ERR_INVALID_ARG, "layer stride smaller than one box or not a multiple of 16 bytes");
+  for (const void* p : {src_k, src_v, stg_k, stg_v, (const void*)dst_k, (const void*)dst_v})
+    if (p && !aligned(p, 16)) return fail(c, BS_ERR_INVALID_ARG, "box pointers must be 16-byte aligned");
+  // destinations pairwise disjoint; no source range of an aliased box meets a destination
+  std::vector<int> order(nseg);
+  for (int i = 0; i < nseg; ++i) order[i] = i;
+  std::sort(order.begin(), order.end(), [&](int x, int y) {
+    return segs[x].dst_row != segs[y].dst_row ? segs[x].dst_row < segs[y].dst_row : segs[x].dst_col < segs[y].dst_col;
+  });
+  for (int t = 1; t < nseg; ++t) {
+    const bs_copy_seg &x = segs[order[t - 1]], &y = segs[order[t]];
+    if (x.len > 0 && y.len > 0 && x.dst_row == y.dst_row && (int64_t)x.dst_col + x.len > y.dst_col)
+      return fail(c, BS_ERR_OVERLAP, "segments %d and %d write overlapping destination cells", order[t - 1], order[t]);
+  }
+  const bool src_alias = any_src && (src_k == dst_k || src_v == dst_v || src_k == dst_v || src_v == dst_k);
+  const bool stg_alias = any_stg && (stg_k == dst_k || stg_v == dst_v || stg_k == dst_v || stg_v == dst_k);
+  if (src_alias || stg_alias) {
+    for (int i = 0; i < nseg; ++i) {
+      const bs_copy_seg& g = segs[i];
+      if (g.len == 0 || (g.src_kind == 0 && !src_alias) || (g.src_kind == 1 && !stg_alias)) continue;
+      for (int jj = 0; jj < nseg; ++jj) {
+        const bs_copy_seg& d = segs[jj];
+        if (d.len == 0 || d.dst_row != g.src_row) continue;
+        if (g.src_col < d.dst_col + d.len && d.dst_col < g.src_col + g.len)
+          return fail(c, BS_ERR_OVERLAP, "segment %d reads cells that segment %d writes", i, jj);
+      }
+    }
+  }
+  if (nseg == 0 || n_layers == 0 || total_chunks == 0) return BS_OK;
+  std::vector<CopyUnit> units;
+  units.reserve((size_t)total_chunks);
+  for (int i = 0; i < nseg; ++i) {
+    const int64_t nc = (segs[i].len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
+    for (int64_t k = 0; k < nc; ++k) units.push_back(CopyUnit{i, (int32_t)k});
+  }
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Blob blob;
+  const size_t off_segs = blob.add(segs, sizeof(bs_copy_seg) * nseg);
+  const size_t off_units = blob.add(units.data(), sizeof(CopyUnit) * units.size());
+  Slot* sl = nullptr;
+  int st = upload(c, s, blob.bytes.data(), blob.bytes.size(), &sl);
+  if (st) return st;
+  const char* base = static_cast<const char*>(sl->d);
+  CopyArgs a{};
+  a.segs = reinterpret_cast<const bs_copy_seg*>(base + off_segs);
+  a.units = reinterpret_cast<const CopyUnit*>(base + off_units);
+  a.n_units = (int)units.size();
+  a.n_layers = n_layers; a.Hkv = Hkv; a.row_bytes = row_bytes;
+  a.src_k = static_cast<const char*>(src_k); a.src_v = static_cast<const char*>(src_v);
+  a.src_ls = src_layer_stride; a.W_src = W_src;
+  a.stg_k = static_cast<const char*>(stg_k); a.stg_v = static_cast<const char*>(stg_v);
+  a.stg_ls = stg_layer_stride; a.W_stg = W_stg;
+  a.dst_k = static_cast<char*>(dst_k); a.dst_v = static_cast<char*>(dst_v);
+  a.dst_ls = dst_layer_stride; a.W_dst = W_dst;
+  hipError_t e = launch_compact(a, s);
+  return finish(c, sl, s, e, "compact launch");
+}
+
+}  // extern "C"

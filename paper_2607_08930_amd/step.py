@@ -1,0 +1,130 @@
+"""One mixed-state denoising step on the GPU, sequenced over the C ABI.
+
+Order (Algorithm 1's block-cycle, one denoising step): gather the active
+blocks' token ids and mask bits -> dual-cache block attention for each layer
+(with the in-place fresh-KV write) -> parallel decode -> scatter tokens and
+mask back into the dense box. At a block boundary ``compact`` first rewrites
+the KV boxes of every layer. PyTorch only provides device memory and the
+stream; every step runs in libblockserve's kernels.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import (BS_BF16, BS_F32, Context, bs_decode_workspace_bytes, bs_dual_cache_block_attention,
+               bs_gather_active_blocks, bs_kv_scatter_compact, bs_parallel_decode,
+               bs_scatter_active_blocks)
+
+
+def dt_code(dtype: str) -> int:
+    return BS_BF16 if dtype == "bf16" else BS_F32
+
+
+def torch_dtype(dtype: str):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def to_device(x: np.ndarray, dtype: str | None = None, device="cuda") -> torch.Tensor:
+    """numpy -> device tensor; bf16 arrives as uint16 bit patterns."""
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+def to_host(t: torch.Tensor) -> np.ndarray:
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+@dataclass
+class Layer:
+    q: torch.Tensor        # [n][L][Hq][D]
+    k_new: torch.Tensor    # [n][L][Hkv][D]
+    v_new: torch.Tensor
+    k_cache: torch.Tensor  # [R][Hkv][W][D]
+    v_cache: torch.Tensor
+    out: torch.Tensor      # [n][L][Hq][D]
+
+
+@dataclass
+class StepState:
+    L: int
+    Hq: int
+    Hkv: int
+    D: int
+    V: int
+    dtype: str
+    R: int
+    W: int
+    tokens: torch.Tensor   # [R][W] int32 (dense box)
+    mask: torch.Tensor     # [R][W] uint8
+    layers: list
+    logits: torch.Tensor   # [n_max][L][V]
+    n_max: int
+    tau: float = 0.9
+    q_min: int = 1
+    eos_id: int = -1
+    write_back: bool = True
+    scale: float = 0.0
+    # compact block state and decode outputs (allocated by ``alloc``)
+    tok_c: torch.Tensor = None
+    msk_c: torch.Tensor = None
+    pos: torch.Tensor = None
+    n_unmasked: torch.Tensor = None
+    done: torch.Tensor = None
+    eos_seen: torch.Tensor = None
+    conf: torch.Tensor = None
+    dec_ws: torch.Tensor = None
+    flags_host: torch.Tensor = None
+    extra: dict = field(default_factory=dict)
+
+    def alloc(self):
+        dev = self.tokens.device
+        n, L = self.n_max, self.L
+        self.tok_c = torch.empty((n, L), dtype=torch.int32, device=dev)
+        self.msk_c = torch.empty((n, L), dtype=torch.uint8, device=dev)
+        self.pos = torch.empty((n, L), dtype=torch.int32, device=dev)
+        self.n_unmasked = torch.empty(n, dtype=torch.int32, device=dev)
+        self.done = torch.empty(n, dtype=torch.uint8, device=dev)
+        self.eos_seen = torch.empty(n, dtype=torch.uint8, device=dev)
+        self.conf = torch.empty((n, L), dtype=torch.float32, device=dev)
+        ws = bs_decode_workspace_bytes(n, L, self.V, dt_code(self.dtype))
+        self.dec_ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
+        return self
+
+
+def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want_conf=False,
+             layers=None) -> None:
+    """Enqueue one step for the requests ``reqs`` (REQ_DTYPE, n <= n_max)."""
+    n = len(reqs)
+    L, R, W = st.L, st.R, st.W
+    dt = dt_code(st.dtype)
+    bs_gather_active_blocks(ctx, reqs, L, R, W, st.tokens, st.tokens.stride(0) * 4, 4, st.tok_c, st.pos,
+                            stream=stream)
+    bs_gather_active_blocks(ctx, reqs, L, R, W, st.mask, st.mask.stride(0), 1, st.msk_c, None, stream=stream)
+    for lay in (st.layers if layers is None else layers):
+        bs_dual_cache_block_attention(ctx, reqs, L, st.Hq, st.Hkv, st.D, dt, st.scale, lay.q, lay.k_new,
+                                      lay.v_new, lay.k_cache, lay.v_cache, R, W, st.write_back, lay.out,
+                                      None, 0, stream=stream)
+    bs_parallel_decode(ctx, reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c, st.tau,
+                       st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen,
+                       st.conf if want_conf else None, st.dec_ws, st.dec_ws.numel(), stream=stream)
+    bs_scatter_active_blocks(ctx, reqs, L, R, W, st.tok_c, 4, st.tokens, st.tokens.stride(0) * 4,
+                             stream=stream)
+    bs_scatter_active_blocks(ctx, reqs, L, R, W, st.msk_c, 1, st.mask, st.mask.stride(0), stream=stream)
+
+
+def compact(ctx: Context, segs: np.ndarray, n_layers: int, Hkv: int, D: int, dtype: str,
+            src_k: torch.Tensor, src_v: torch.Tensor, stg_k: torch.Tensor, stg_v: torch.Tensor,
+            dst_k: torch.Tensor, dst_v: torch.Tensor, stream=None) -> None:
+    """KV boxes are [layers][R][Hkv][W][D] tensors; strides come from them."""
+    eb = src_k.element_size()
+    bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt_code(dtype), src_k, src_v, src_k.stride(0) * eb,
+                          src_k.shape[1], src_k.shape[3], stg_k, stg_v,
+                          stg_k.stride(0) * eb if stg_k is not None else 0,
+                          stg_k.shape[1] if stg_k is not None else 1, stg_k.shape[3] if stg_k is not None else 1,
+                          dst_k, dst_v, dst_k.stride(0) * eb, dst_k.shape[1], dst_k.shape[3], stream=stream)

@@ -1,0 +1,82 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/blockserve.h declares, validates descriptors on the
+host, and rejects bad arguments before touching a device."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2607_08930_amd as bs
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "blockserve.h")
+
+
+def declared():
+    src = open(HDR).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bs_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared()
+    assert len(names) >= 12
+    out = subprocess.run(["nm", "-D", "--defined-only", bs.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\sT\s(bs_\w+)", out))
+    for n in names:
+        assert n in exported, f"{n} declared but not exported"
+        assert hasattr(bs.lib, n)
+        assert hasattr(bs, n), f"binding lacks {n}"
+
+
+def test_status_strings():
+    assert [bs.bs_status_string(i) for i in range(7)] == [
+        "BS_OK", "BS_ERR_INVALID_ARG", "BS_ERR_UNSUPPORTED", "BS_ERR_DESCRIPTOR", "BS_ERR_OVERLAP",
+        "BS_ERR_WORKSPACE", "BS_ERR_HIP"]
+    assert bs.bs_status_string(99) == "BS_UNKNOWN_STATUS"
+
+
+@pytest.mark.parametrize("bad,msg", [
+    ((5, 16, 2, 0, 0), "block index"), ((5, 16, -1, 0, 0), "block index"), ((5, 0, 0, 0, 0), "g >= 1"),
+    ((-1, 16, 0, 0, 0), "p >= 0"), ((5, 16, 0, 9, 0), "row 9"), ((5, 16, 0, 0, 40), "exceeds W"),
+    ((5, 16, 0, 0, -1), "exceeds W"),
+])
+def test_validate_rejects_each_class(bad, msg):
+    with pytest.raises(bs.BlockServeError, match=msg) as e:
+        bs.bs_validate_requests(np.array([bad], bs.REQ_DTYPE), 8, 4, 52)
+    assert e.value.name == "BS_ERR_DESCRIPTOR"
+
+
+def test_validate_duplicate_row_and_good_batch():
+    with pytest.raises(bs.BlockServeError, match="used twice"):
+        bs.bs_validate_requests(np.array([(5, 16, 0, 1, 0), (5, 16, 0, 1, 0)], bs.REQ_DTYPE), 8, 4, 52)
+    good = np.array([(5, 16, 1, 0, 31), (12, 24, 0, 1, 16), (7, 8, 0, 2, 37), (20, 32, 3, 3, 0)], bs.REQ_DTYPE)
+    bs.bs_validate_requests(good, 8, 4, 52)
+    with pytest.raises(bs.BlockServeError, match="L < 1"):
+        bs.bs_validate_requests(good, 0, 4, 52)
+
+
+def test_calls_without_context_fail_before_any_device_work():
+    null = None
+    assert bs.lib.bs_gather_active_blocks(null, None, 0, 8, 1, 1, None, 0, 4, None, None, None) == 1
+    assert bs.lib.bs_parallel_decode(null, None, 0, 8, 10, 0, None, 16, None, None, 0.9, 1, -1, None, None,
+                                     None, None, None, 0, None) == 1
+    assert bs.lib.bs_kv_scatter_compact(null, None, 0, 1, 1, 8, 0, None, None, 0, 1, 1, None, None, 0, 1, 1,
+                                        None, None, 0, 1, 1, None) == 1
+    assert "ctx is NULL" in bs.bs_last_error()
+
+
+def test_workspace_queries():
+    assert bs.bs_decode_workspace_bytes(32, 32, 126464, bs.BS_BF16) == 32 * 32 * 4 * 16
+    assert bs.bs_decode_workspace_bytes(4, 8, 1000, bs.BS_F32) == 4 * 8 * 1 * 16
+    assert bs.bs_decode_workspace_bytes(0, 8, 1000, bs.BS_F32) == 0
+    reqs = np.array([(5, 16, 1, 0, 31)], bs.REQ_DTYPE)
+    assert bs.bs_attention_workspace_bytes(reqs, 8, 2, 2, 64, bs.BS_F32) >= 0
+
+
+def test_package_has_no_cpu_fallback():
+    import inspect
+    src = inspect.getsource(bs)
+    assert "oracle" not in src.replace("oracle/", "")
+    assert "import synth" not in src

@@ -1,0 +1,282 @@
+"""GPU parity: every HIP entry point against the fp64 oracle on the same
+seeded inputs (element by element; integer outputs bit-exact outside the
+reported exemption set; attention within the stated tolerances)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import (ATT_TOL, check_attention, check_decode, exempt_requests, lazy, run_attention,
+                      run_decode, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    torch, bs, _ = lazy()
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    c = bs.Context(0)
+    yield c
+    c.close()
+
+
+# ---------------------------------------------------------------- K1 gather / scatter
+@pytest.mark.parametrize("eb", [1, 2, 4, 8, 16])
+def test_gather_scatter_bit_exact(ctx, eb):
+    torch, bs, bstep = lazy()
+    say(f"[gather eb={eb}]")
+    w = synth.custom(8, 2, 2, 16, 50, "f32", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8], [1, 0, 1, 2, 0],
+                     W=40, rows=[2, 0, 4, 1, 3])
+    rng = np.random.default_rng(eb)
+    box = rng.integers(0, 256, size=(w.R, w.W, eb), dtype=np.uint8)
+    ref, pos_ref = oracle.gather_active_blocks(w.reqs, w.L, box)
+    dbox = torch.from_numpy(box).cuda()
+    dst = torch.full((w.n, w.L, eb), 0xAB, dtype=torch.uint8, device="cuda")
+    pos = torch.full((w.n, w.L), -9, dtype=torch.int32, device="cuda")
+    bs.bs_gather_active_blocks(ctx, w.reqs, w.L, w.R, w.W, dbox, w.W * eb, eb, dst, pos)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dst.cpu().numpy(), ref)
+    np.testing.assert_array_equal(pos.cpu().numpy(), pos_ref)
+    y = rng.integers(0, 256, size=(w.n, w.L, eb), dtype=np.uint8)
+    exp = oracle.scatter_active_blocks(w.reqs, w.L, y, box)
+    bs.bs_scatter_active_blocks(ctx, w.reqs, w.L, w.R, w.W, torch.from_numpy(y).cuda(), eb, dbox, w.W * eb)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dbox.cpu().numpy(), exp)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_gather_scatter_workloads(ctx, cfg):
+    torch, bs, bstep = lazy()
+    say(f"[gather cfg{cfg}]")
+    w = synth.workload(cfg)
+    tok, msk, blk = synth.gen_state(w)
+    for arr, eb in ((tok, 4), (msk, 1)):
+        ref, pos_ref = oracle.gather_active_blocks(w.reqs, w.L, arr)
+        d = torch.from_numpy(arr).cuda()
+        out = torch.empty((w.n, w.L), dtype=d.dtype, device="cuda")
+        pos = torch.empty((w.n, w.L), dtype=torch.int32, device="cuda")
+        bs.bs_gather_active_blocks(ctx, w.reqs, w.L, w.R, w.W, d, w.W * eb, eb, out, pos)
+        bs.bs_scatter_active_blocks(ctx, w.reqs, w.L, w.R, w.W, out, eb, d, w.W * eb)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(out.cpu().numpy(), ref)
+        np.testing.assert_array_equal(pos.cpu().numpy(), pos_ref)
+        np.testing.assert_array_equal(d.cpu().numpy(), arr)   # scatter(gather(X)) = X
+    assert np.array_equal(oracle.gather_active_blocks(w.reqs, w.L, msk)[0].astype(bool), blk)
+
+
+def test_gather_empty_batch_is_noop(ctx):
+    torch, bs, _ = lazy()
+    d = torch.zeros((2, 8), dtype=torch.int32, device="cuda")
+    bs.bs_gather_active_blocks(ctx, np.zeros(0, bs.REQ_DTYPE), 8, 2, 8, d, 32, 4, d, None)
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- K3 decode
+def _decode_case(ctx, w, label, tau=None, q_min=None, eos_id=None):
+    tok, msk, blk = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    assert np.array_equal(msk_c.astype(bool), blk)
+    logits = synth.gen_logits(w, blk)
+    say(f"[decode {label}] n={w.n} V={w.V} masked={int(blk.sum())}")
+    got = run_decode(ctx, w, logits, tok_c, msk_c, tau=tau, q_min=q_min, eos_id=eos_id)
+    ref = oracle.parallel_decode(w.reqs, w.L, logits, tok_c, msk_c, tau=w.tau if tau is None else tau,
+                                 q_min=w.q_min if q_min is None else q_min,
+                                 eos_id=w.eos_id if eos_id is None else eos_id, dtype=w.dtype)
+    nex = check_decode(w, got, ref, tau=tau, label=label)
+    say(f"  exempt requests: {nex} of {w.n}")
+    return got, ref, nex
+
+
+def test_decode_tiny_fp32(ctx):
+    _decode_case(ctx, synth.workload(1), "cfg1")
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_decode_full_size(ctx, cfg):
+    _, _, nex = _decode_case(ctx, synth.workload(cfg), f"cfg{cfg}")
+    assert nex <= synth.workload(cfg).n // 4
+
+
+def test_decode_every_argmax_bit_exact(ctx):
+    # tau below every confidence selects every masked position: tokens = argmax
+    w = synth.workload(2)
+    got, ref, nex = _decode_case(ctx, w, "cfg2 tau=-1", tau=-1.0)
+    assert nex == 0
+    assert (got["masked"] == 0).all()
+
+
+def test_decode_fixed_quota_and_eos(ctx):
+    w = synth.custom(8, 2, 2, 16, 300, "bf16", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8], [1, 0, 1, 2, 0],
+                     W=40, logits="spiked")
+    for q in (1, 2, 3):
+        _decode_case(ctx, w, f"quota q={q}", tau=1.5, q_min=q)
+    got, ref, _ = _decode_case(ctx, w, "eos", eos_id=0)
+
+
+def test_decode_tiny_vocab_tail(ctx):
+    # V not a multiple of the vector width exercises the element-wise tail
+    w = synth.custom(8, 2, 2, 16, 37, "f32", [3, 7], [16, 12], [1, 1], logits="normal", logit_sigma=2.0)
+    _decode_case(ctx, w, "V=37 fp32")
+    w = synth.custom(8, 2, 2, 16, 70000, "bf16", [3, 7], [16, 12], [1, 1])
+    _decode_case(ctx, w, "V=70000 bf16 (3 chunks, ragged)")
+
+
+def test_decode_rejects_unaligned_row_stride(ctx):
+    torch, bs, bstep = lazy()
+    w = synth.custom(8, 2, 2, 16, 300, "bf16", [3], [16], [1])
+    dl = torch.zeros((1, 8, 300), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(bs.BlockServeError, match="multiple of 16 bytes"):
+        run_decode(ctx, w, None, np.zeros((1, 8), np.int32), np.ones((1, 8), np.uint8), dev_logits=dl)
+
+
+def test_decode_rejects_zero_quota(ctx):
+    torch, bs, _ = lazy()
+    w = synth.workload(1)
+    with pytest.raises(bs.BlockServeError, match="INVALID_ARG"):
+        run_decode(ctx, w, np.zeros((w.n, w.L, w.V), np.float32), np.zeros((w.n, w.L), np.int32),
+                   np.ones((w.n, w.L), np.uint8), q_min=0)
+
+
+# ---------------------------------------------------------------- K2 attention
+def _att(ctx, w, label, **kw):
+    say(f"[attention {label}] n={w.n} Hq={w.Hq} Hkv={w.Hkv} D={w.D} {w.dtype}")
+    got, kc2, vc2, inp = run_attention(ctx, w, **kw)
+    ref, kcr, vcr = oracle.dual_cache_block_attention(w.reqs, w.L, inp["q"], inp["k_new"], inp["v_new"],
+                                                      inp["k_cache"], inp["v_cache"], dtype=w.dtype,
+                                                      write_back=kw.get("write_back", True))
+    err, mx = check_attention(w, got, ref, label=label)
+    say(f"  max abs err {err:.3e}, max |O| {mx:.3e}")
+    np.testing.assert_array_equal(kc2, kcr)
+    np.testing.assert_array_equal(vc2, vcr)
+    return got, ref
+
+
+def test_attention_tiny_fp32(ctx):
+    _att(ctx, synth.workload(1), "cfg1")
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_attention_full_size(ctx, cfg):
+    _att(ctx, synth.workload(cfg), f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_attention_peaked_scores(ctx, cfg):
+    # Q ~ N(0, 8^2): scores are far from uniform, so the online-softmax
+    # rescaling is exercised
+    _att(ctx, synth.workload(cfg, variant=1, q_sigma=8.0), f"cfg{cfg} peaked")
+
+
+def test_attention_skewed_budget(ctx):
+    _att(ctx, synth.workload(4), "cfg4")
+
+
+def test_attention_edge_geometries(ctx):
+    # partial last blocks, empty prompt, empty suffix, rows out of order, D=64,
+    # L=8 and L=64 (two row blocks per head), GQA and MHA
+    cases = [
+        ("bf16 L8 partial", synth.custom(8, 4, 2, 128, 10, "bf16", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8],
+                                          [1, 0, 1, 2, 0], W=40, rows=[2, 0, 4, 1, 3], kv_sigma=0.1)),
+        ("bf16 D64 G3", synth.custom(32, 6, 2, 64, 10, "bf16", [0, 37, 100], [70, 64, 33], [2, 1, 1],
+                                      rows=[1, 2, 0], kv_sigma=0.1)),
+        ("bf16 L64 G4", synth.custom(64, 8, 2, 128, 10, "bf16", [10, 200], [130, 64], [2, 0], kv_sigma=0.1,
+                                      q_sigma=3.0)),
+        ("bf16 G7 L32", synth.custom(32, 28, 4, 128, 10, "bf16", [1, 700], [40, 512], [1, 15], kv_sigma=0.1,
+                                      q_sigma=4.0)),
+        ("fp32 D128 G2", synth.custom(16, 4, 2, 128, 10, "f32", [3, 40], [20, 33], [1, 2])),
+    ]
+    for label, w in cases:
+        _att(ctx, w, label)
+
+
+def test_attention_poisoned_padding_and_stale_slot(ctx):
+    for cfg in (1, 2):
+        w = synth.workload(cfg)
+        a, _, _, _ = run_attention(ctx, w)
+        b, _, _, _ = run_attention(ctx, w, poison=True)
+        say(f"[attention poison cfg{cfg}]")
+        assert np.array_equal(a, b)
+
+
+def test_attention_no_write_back_leaves_cache(ctx):
+    w = synth.workload(2)
+    _att(ctx, w, "cfg2 read-only", write_back=False)
+
+
+def test_attention_batch_invariance_and_determinism(ctx):
+    w = synth.workload(3)
+    full, _, _, inp = run_attention(ctx, w)
+    again, _, _, _ = run_attention(ctx, w)
+    assert np.array_equal(full, again), "run-to-run results differ"
+    for i in (0, 17, 63):
+        one, _, _, _ = run_attention(ctx, w, reqs=w.reqs[i:i + 1], q=inp["q"][i:i + 1],
+                                     kn=inp["k_new"][i:i + 1], vn=inp["v_new"][i:i + 1],
+                                     kc=inp["k_cache"], vc=inp["v_cache"])
+        assert np.array_equal(one[0], full[i]), f"request {i} alone differs from in-batch"
+    perm = np.random.default_rng(0).permutation(w.n)
+    pm, _, _, _ = run_attention(ctx, w, reqs=w.reqs[perm], q=inp["q"][perm], kn=inp["k_new"][perm],
+                                vn=inp["v_new"][perm], kc=inp["k_cache"], vc=inp["v_cache"])
+    assert np.array_equal(pm, full[perm]), "permuted batch differs"
+
+
+def test_attention_rejects_unsupported(ctx):
+    torch, bs, _ = lazy()
+    w = synth.custom(64, 28, 4, 128, 10, "bf16", [3], [64], [0])   # 7 heads x 2 row blocks > 8 waves
+    with pytest.raises(bs.BlockServeError, match="UNSUPPORTED"):
+        run_attention(ctx, w)
+    w = synth.custom(32, 3, 2, 128, 10, "bf16", [3], [64], [0])    # Hq % Hkv != 0
+    with pytest.raises(bs.BlockServeError, match="UNSUPPORTED"):
+        run_attention(ctx, w)
+
+
+# ---------------------------------------------------------------- K4 compaction
+def test_compact_stable_slot_plan(ctx):
+    torch, bs, bstep = lazy()
+    say("[compact stable-slot]")
+    rng = np.random.default_rng(4)
+    layers, R, H, W, D = 3, 6, 2, 40, 64
+    ck = rng.integers(0, 2**16, size=(layers, R, H, W, D), dtype=np.uint16)
+    cv = rng.integers(0, 2**16, size=(layers, R, H, W, D), dtype=np.uint16)
+    sk = rng.integers(0, 2**16, size=(layers, 3, H, W, D), dtype=np.uint16)
+    sv = rng.integers(0, 2**16, size=(layers, 3, H, W, D), dtype=np.uint16)
+    segs = np.array([(1, 0, 0, 1, W - 17, 17), (1, 2, 0, 4, 0, 40), (0, 5, 10, 3, 2, 30), (1, 1, 3, 0, 30, 1)],
+                    dtype=synth.SEG_DTYPE)
+    ek, ev = oracle.kv_scatter_compact(segs, ck, cv, sk, sv, ck, cv)
+    d = {k: bstep.to_device(v, "bf16") for k, v in dict(ck=ck, cv=cv, sk=sk, sv=sv).items()}
+    bstep.compact(ctx, segs, layers, H, D, "bf16", d["ck"], d["cv"], d["sk"], d["sv"], d["ck"], d["cv"])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bstep.to_host(d["ck"]), ek)
+    np.testing.assert_array_equal(bstep.to_host(d["cv"]), ev)
+
+
+def test_compact_round_trip_out_of_place(ctx):
+    torch, bs, bstep = lazy()
+    say("[compact round trip]")
+    rng = np.random.default_rng(5)
+    layers, R, H, W, D = 2, 5, 4, 33, 128
+    ok_ = rng.standard_normal((layers, R, H, W, D)).astype(np.float32)
+    ov = rng.standard_normal((layers, R, H, W, D)).astype(np.float32)
+    live = [(0, 7), (2, 33), (4, 5)]
+    fwd = np.array([(0, r, W - ln, t, W - ln, ln) for t, (r, ln) in enumerate(live)], dtype=synth.SEG_DTYPE)
+    dk, dv = bstep.to_device(ok_), bstep.to_device(ov)
+    nk = torch.zeros((layers, 3, H, W, D), device="cuda")
+    nv = torch.zeros_like(nk)
+    bstep.compact(ctx, fwd, layers, H, D, "f32", dk, dv, None, None, nk, nv)
+    ek, ev = oracle.kv_scatter_compact(fwd, ok_, ov, None, None, np.zeros((layers, 3, H, W, D), np.float32),
+                                       np.zeros((layers, 3, H, W, D), np.float32))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(nk.cpu().numpy(), ek)
+    np.testing.assert_array_equal(nv.cpu().numpy(), ev)
+
+
+def test_compact_rejects_overlap(ctx):
+    torch, bs, bstep = lazy()
+    box = torch.zeros((1, 2, 1, 8, 8), device="cuda")
+    segs = np.array([(0, 0, 0, 1, 0, 5), (0, 0, 0, 1, 4, 3)], dtype=synth.SEG_DTYPE)
+    with pytest.raises(bs.BlockServeError, match="OVERLAP"):
+        bstep.compact(ctx, segs, 1, 1, 8, "f32", box, box, None, None, box.clone(), box.clone())
+    segs = np.array([(0, 0, 2, 0, 0, 4)], dtype=synth.SEG_DTYPE)
+    with pytest.raises(bs.BlockServeError, match="OVERLAP"):
+        bstep.compact(ctx, segs, 1, 1, 8, "f32", box, box, None, None, box, box)

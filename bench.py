@@ -5,8 +5,10 @@ layer) -> parallel decode -> scatter (token ids, mask bits), all through
 libblockserve's C ABI on one stream; the block-boundary churn workload (5)
 adds the KV compaction first. Inputs are synthetic and resident in HBM before
 timing. Between steps (outside the per-step events) the decoded token/mask
-state is restored from pristine copies and a 512 MiB buffer is overwritten so
-the 256 MB Infinity Cache holds none of the step's data (cold numbers).
+state is restored from pristine copies and a 512 MiB buffer is read, so the
+256 MB Infinity Cache holds none of the step's data (cold numbers). The sweep
+reads rather than writes: a written sweep would leave the cache full of dirty
+lines whose write-back would then be charged to the timed step.
 
 Prints ONE JSON line (rank 0): positions/s, ms per step, per-kernel event
 times, algorithmic HBM traffic, the roofline of the dominant kernel and the
@@ -123,7 +125,7 @@ def main():
     small_bytes = ab["positions"] * (5 + 5 + 4 + 5 + 5)
     step_bytes = ab["attn"] + logits_bytes + small_bytes
     tok0, msk0 = st.tokens.clone(), st.mask.clone()
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")    # 512 MiB, swept by reading
     stream = torch.cuda.current_stream()
     ctx = bs.Context(0)
 
@@ -133,8 +135,8 @@ def main():
         L, R, W = st.L, st.R, st.W
         dt = bstep.dt_code(st.dtype)
         if evs: evs[0].record(stream)
-        bs.bs_gather_active_blocks(ctx, w.reqs, L, R, W, st.tokens, W * 4, 4, st.tok_c, st.pos)
-        bs.bs_gather_active_blocks(ctx, w.reqs, L, R, W, st.mask, W, 1, st.msk_c, None)
+        bs.bs_gather_active_blocks_n(ctx, w.reqs, L, R, W, [st.tokens, st.mask], [W * 4, W], [4, 1],
+                                     [st.tok_c, st.msk_c], st.pos)
         if evs: evs[1].record(stream)
         for lay in st.layers:
             bs.bs_dual_cache_block_attention(ctx, w.reqs, L, st.Hq, st.Hkv, st.D, dt, 0.0, lay.q, lay.k_new,
@@ -144,15 +146,15 @@ def main():
                               st.tau, st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, None,
                               st.dec_ws, st.dec_ws.numel())
         if evs: evs[3].record(stream)
-        bs.bs_scatter_active_blocks(ctx, w.reqs, L, R, W, st.tok_c, 4, st.tokens, W * 4)
-        bs.bs_scatter_active_blocks(ctx, w.reqs, L, R, W, st.msk_c, 1, st.mask, W)
+        bs.bs_scatter_active_blocks_n(ctx, w.reqs, L, R, W, [st.tok_c, st.msk_c], [4, 1], [st.tokens, st.mask],
+                                      [W * 4, W])
         if evs: evs[4].record(stream)
 
     def reset():
         st.tokens.copy_(tok0)
         st.mask.copy_(msk0)
         if not args.warm:
-            flush.zero_()
+            flush.sum()
 
     for _ in range(args.warmup):
         reset()
@@ -194,7 +196,7 @@ def main():
         "config": {"workload": w.name, "n_requests": w.n, "positions_per_step": ab["positions"],
                    "masked_rows": nmask, "L": w.L, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "V": w.V,
                    "layers": w.layers, "sum_len": int((w.reqs["p"] + w.reqs["g"]).sum()),
-                   "cache": "warm" if args.warm else "cold (512 MiB flush between steps)"},
+                   "cache": "warm" if args.warm else "cold (512 MiB read sweep between steps)"},
         "hbm": {"algorithmic_bytes_per_step": step_bytes, "achieved_GBps": round(step_bytes / (ms / 1e3) / 1e9, 1),
                 "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
         "kernels_ms": {n_: round(float(np.median(per[:, i])), 5) for i, n_ in enumerate(names)},

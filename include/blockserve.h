@@ -123,6 +123,19 @@ int bs_scatter_active_blocks(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L,
                              const void* src_compact, int elem_bytes, void* dst_dense,
                              int64_t dst_row_stride_bytes, void* stream);
 
+/* K1 over several same-geometry tensors in one launch (the step gathers token
+ * ids and mask bits together). Tensor k (0 <= k < ntensors <= 4) has its own
+ * element size elem_bytes[k], dense row stride *_row_stride_bytes[k], dense
+ * pointer and compact pointer; each is moved exactly as by the single-tensor
+ * call above. The four arrays are host arrays of ntensors entries, read
+ * before the call returns. pos_out as above (gather only). */
+int bs_gather_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W, int ntensors,
+                              const void* const* src, const int64_t* src_row_stride_bytes,
+                              const int* elem_bytes, void* const* dst, int32_t* pos_out, void* stream);
+int bs_scatter_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W, int ntensors,
+                               const void* const* src_compact, const int* elem_bytes, void* const* dst_dense,
+                               const int64_t* dst_row_stride_bytes, void* stream);
+
 /*
  * K2 -- dual-cache block attention for one layer (paragraph "Vectorized
  * mixed-schedule execution": the active block is computed against the cached
@@ -177,8 +190,10 @@ int bs_dual_cache_block_attention(bs_ctx* ctx, const bs_req_desc* reqs, int n, i
  * j in M are read; they must be finite. tokens [n][L] int32 and masked [n][L]
  * uint8 are updated in place. q_min >= 1 (at least one unmask per step while
  * any position is masked); L <= 64.
- * ws: device workspace of at least bs_decode_workspace_bytes(...) bytes; its
- * contents need no initialisation.
+ * ws: device workspace of at least bs_decode_workspace_bytes(...) bytes,
+ * 16-byte aligned; its contents on entry are ignored (it carries per-row
+ * partial results between the call's two launches). Calls that may overlap
+ * (different streams) need different workspaces.
  */
 size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype logits_dt);
 int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V,

@@ -20,7 +20,8 @@ import numpy as np
 __all__ = [
     "REQ_DTYPE", "SEG_DTYPE", "BS_F32", "BS_BF16", "BlockServeError", "Context", "lib", "LIB_PATH",
     "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
-    "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_attention_workspace_bytes",
+    "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_gather_active_blocks_n",
+    "bs_scatter_active_blocks_n", "bs_attention_workspace_bytes",
     "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
     "bs_kv_scatter_compact",
 ]
@@ -71,6 +72,8 @@ _SIGS = {
     "bs_validate_requests": (_i32, [_vp, _i32, _i32, _i32, _i32]),
     "bs_gather_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _i32, _vp, _vp, _vp]),
     "bs_scatter_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i64, _vp]),
+    "bs_gather_active_blocks_n": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "bs_scatter_active_blocks_n": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "bs_attention_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "bs_dual_cache_block_attention": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                              _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
@@ -192,6 +195,35 @@ def bs_scatter_active_blocks(ctx, reqs, L, R, W, src_compact, elem_bytes, dst_de
     return _check(lib.bs_scatter_active_blocks(_ptr(ctx), _ptr(r), len(r), L, R, W, _ptr(src_compact),
                                                elem_bytes, _ptr(dst_dense), dst_row_stride_bytes,
                                                _stream(stream)), ctx)
+
+
+def _tensor_arrays(ptrs, strides, elem_bytes):
+    k = len(ptrs)
+    if not (len(strides) == len(elem_bytes) == k):
+        raise ValueError("pointer, stride and element-size lists differ in length")
+    P = (_vp * max(k, 1))(*[_ptr(x) for x in ptrs])
+    S = (_i64 * max(k, 1))(*strides)
+    E = (_i32 * max(k, 1))(*elem_bytes)
+    return P, S, E
+
+
+def bs_gather_active_blocks_n(ctx, reqs, L, R, W, src, src_row_stride_bytes, elem_bytes, dst, pos_out=None,
+                              stream=None):
+    """``src``/``dst``/``src_row_stride_bytes``/``elem_bytes`` are equal-length lists."""
+    r = _host(reqs, REQ_DTYPE)
+    P, S, E = _tensor_arrays(src, src_row_stride_bytes, elem_bytes)
+    D = (_vp * max(len(dst), 1))(*[_ptr(x) for x in dst])
+    return _check(lib.bs_gather_active_blocks_n(_ptr(ctx), _ptr(r), len(r), L, R, W, len(src), P, S, E, D,
+                                                _ptr(pos_out), _stream(stream)), ctx)
+
+
+def bs_scatter_active_blocks_n(ctx, reqs, L, R, W, src_compact, elem_bytes, dst_dense, dst_row_stride_bytes,
+                               stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    P, S, E = _tensor_arrays(dst_dense, dst_row_stride_bytes, elem_bytes)
+    C = (_vp * max(len(src_compact), 1))(*[_ptr(x) for x in src_compact])
+    return _check(lib.bs_scatter_active_blocks_n(_ptr(ctx), _ptr(r), len(r), L, R, W, len(src_compact), C, E,
+                                                 P, S, _stream(stream)), ctx)
 
 
 def bs_attention_workspace_bytes(reqs, L, Hq, Hkv, D, dt) -> int:

@@ -32,22 +32,18 @@ __device__ inline v4u ld16(const void* p) { return *reinterpret_cast<const v4u*>
 __device__ inline void st16(void* p, v4u v) { *reinterpret_cast<v4u*>(p) = v; }
 
 // ---------------------------------------------------------------- attention
-// One work item = (request, KV head, key range [t0, t1) of the logical row).
-// Items with nsplit > 1 write unnormalised partials that a merge pass combines.
+// One work item = (request, KV head) with the request's geometry resolved on
+// the host, so a workgroup needs a single scalar load before its first DMA.
 struct AttnItem {
-  int32_t req;
-  int32_t kvh;
-  int32_t t0;
-  int32_t t1;
-  int32_t split;   // index of this range among the request's ranges
-  int32_t nsplit;  // number of ranges of this request (1: write out directly)
-  int32_t ws_slot; // first partial slot of this request (nsplit > 1)
+  int32_t req;   // request index (row of q / k_new / v_new / out)
+  int32_t kvh;   // KV head
+  int32_t len;   // logical row length p + g (keys [0, len))
+  int32_t s;     // first block position
+  int32_t B;     // block length
+  int32_t row;   // dense row of the cache
+  int32_t off;   // column of logical position 0
   int32_t pad;
 };
-
-// Key range length of one split of the bf16 path. Fixed, so the split count of
-// a request depends on its own length only (bitwise batch invariance).
-constexpr int kAttnSplitKeys = 1024;
 
 struct AttnArgs {
   const bs_req_desc* reqs;
@@ -64,27 +60,34 @@ struct AttnArgs {
   void* v_cache;
   void* out;
   int write_back;
-  // split partials: per slot [L][Hq-group rows][D] fp32 O plus m and l
-  float* ws_o;
-  float* ws_ml;
 };
 
 hipError_t launch_attn_f32(const AttnArgs& a, int n_req, hipStream_t s);
-hipError_t launch_attn_bf16(const AttnArgs& a, int n_req, int n_slots, hipStream_t s);
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- decode
 struct DecPartial {
-  float m;    // chunk max
-  float s;    // sum exp(x - m) over the chunk
+  float m;    // max over the part
+  float s;    // sum exp(x - m) over the part
   int32_t a;  // smallest index attaining m
   int32_t pad;
 };
 
-constexpr int kDecChunkBytes = 65536;  // logits bytes per row chunk (one workgroup)
+constexpr int kDecChunkBytes = 32768;  // logits bytes streamed per chunk of a row
+constexpr int kDecPartChunks = 2;      // chunks per part: one workgroup streams one part of a row
+
+// Parts a row of V elements of `eb` bytes is split into.
+inline int dec_parts(int V, int eb) {
+  const int64_t chunks = ((int64_t)V * eb + kDecChunkBytes - 1) / kDecChunkBytes;
+  return (int)((chunks + kDecPartChunks - 1) / kDecPartChunks);
+}
+
+// Decode workspace: [n * L * parts] DecPartial part results.
+inline size_t dec_workspace_bytes(int n, int L, int parts) { return (size_t)n * L * parts * sizeof(DecPartial); }
 
 struct DecArgs {
   const bs_req_desc* reqs;
-  int n, L, V, nchunk;
+  int n, L, V;
   const void* logits;
   int64_t row_stride;  // elements
   int32_t* tokens;
@@ -95,16 +98,25 @@ struct DecArgs {
   uint8_t* done;
   uint8_t* eos_seen;
   float* conf_out;
+  int parts;       // parts per row
   DecPartial* part;
 };
 
 hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s);
 
 // ---------------------------------------------------------------- gather / scatter
-hipError_t launch_gather(const bs_req_desc* reqs, int n, int L, const void* src, int64_t stride,
-                         int eb, void* dst, int32_t* pos, hipStream_t s);
-hipError_t launch_scatter(const bs_req_desc* reqs, int n, int L, const void* src, int eb,
-                          void* dst, int64_t stride, hipStream_t s);
+constexpr int kMaxGather = 4;  // tensors moved by one gather/scatter launch
+
+struct GatherSet {
+  int count;
+  const void* dense[kMaxGather];   // [R][W] tensors (written by scatter)
+  void* compact[kMaxGather];       // [n][L] tensors (written by gather)
+  int64_t stride[kMaxGather];      // dense row stride in bytes
+  int eb[kMaxGather];              // element bytes: 1, 2, 4, 8 or 16
+};
+
+hipError_t launch_gather(const bs_req_desc* reqs, int n, int L, const GatherSet& g, int32_t* pos, hipStream_t s);
+hipError_t launch_scatter(const bs_req_desc* reqs, int n, int L, const GatherSet& g, hipStream_t s);
 
 // ---------------------------------------------------------------- compaction
 struct CopyUnit {

@@ -17,12 +17,19 @@ namespace {
 
 constexpr int kSlots = 16;
 
+// An upload slot holds one device blob (descriptors plus the work list derived
+// from them) and the host key it was built from. The key is the small input
+// the blob is a function of (call kind, shape parameters, descriptor bytes), so
+// a repeated call (every denoising step of a block-cycle repeats its
+// descriptors) finds its blob by comparing the key alone and neither rebuilds
+// nor re-uploads anything.
 struct Slot {
-  void* d = nullptr;       // device copy
+  void* d = nullptr;       // device copy of the blob
   void* h = nullptr;       // pinned staging copy (immutable while live)
   size_t cap = 0;
-  size_t nbytes = 0;
+  std::vector<unsigned char> key;
   uint64_t hash = 0;
+  int meta[4] = {0, 0, 0, 0};  // blob layout (offsets, counts) recorded at build time
   hipEvent_t ready = nullptr;  // recorded after the upload
   hipEvent_t done = nullptr;   // recorded after the last launch that read it
   hipStream_t stream = nullptr;
@@ -102,11 +109,39 @@ int check_reqs(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// Upload `n` bytes of host data; reuses a live slot with identical contents.
-int upload(bs_ctx* c, hipStream_t s, const void* data, size_t n, Slot** out) {
-  const uint64_t hv = fnv1a(data, n);
+// Blob = descriptors followed by an optional work list, 16-byte aligned parts.
+struct Blob {
+  std::vector<unsigned char> bytes;
+  int meta[4] = {0, 0, 0, 0};
+  size_t add(const void* p, size_t n) {
+    size_t off = (bytes.size() + 15) & ~size_t(15);
+    bytes.resize(off + n);
+    if (n) std::memcpy(bytes.data() + off, p, n);
+    return off;
+  }
+};
+
+// Key of a call: a tag and shape parameters, followed by the descriptor bytes.
+struct Key {
+  std::vector<unsigned char> b;
+  Key(char tag, std::initializer_list<int64_t> params, const void* data, size_t n) {
+    b.push_back(static_cast<unsigned char>(tag));
+    for (int64_t v : params) push(&v, sizeof v);
+    push(data, n);
+  }
+  void push(const void* p, size_t n) {
+    const unsigned char* q = static_cast<const unsigned char*>(p);
+    b.insert(b.end(), q, q + n);
+  }
+};
+
+// Find the slot built from `key`, or build the blob with make(Blob&) and
+// upload it into the least recently used slot.
+template <class Make>
+int upload(bs_ctx* c, hipStream_t s, const Key& key, Make make, Slot** out) {
+  const uint64_t hv = fnv1a(key.b.data(), key.b.size());
   for (Slot& sl : c->slots) {
-    if (sl.live && sl.hash == hv && sl.nbytes == n && std::memcmp(sl.h, data, n) == 0) {
+    if (sl.live && sl.hash == hv && sl.key == key.b) {
       if (sl.stream != s) {
         hipError_t e = hipStreamWaitEvent(s, sl.done, 0);
         if (e != hipSuccess) return hip_fail(c, e, "hipStreamWaitEvent");
@@ -116,6 +151,9 @@ int upload(bs_ctx* c, hipStream_t s, const void* data, size_t n, Slot** out) {
       return BS_OK;
     }
   }
+  Blob blob;
+  make(blob);
+  const size_t n = blob.bytes.size();
   Slot& sl = c->slots[c->next];
   c->next = (c->next + 1) % kSlots;
   if (sl.live) {
@@ -141,17 +179,24 @@ int upload(bs_ctx* c, hipStream_t s, const void* data, size_t n, Slot** out) {
     if (e == hipSuccess) e = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming);
     if (e != hipSuccess) return hip_fail(c, e, "hipEventCreate");
   }
-  std::memcpy(sl.h, data, n);
+  std::memcpy(sl.h, blob.bytes.data(), n);
   hipError_t e = hipMemcpyAsync(sl.d, sl.h, n, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync(upload)");
   e = hipEventRecord(sl.ready, s);
   if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+  sl.key = key.b;
   sl.hash = hv;
-  sl.nbytes = n;
+  std::memcpy(sl.meta, blob.meta, sizeof sl.meta);
   sl.stream = s;
   sl.live = true;
   *out = &sl;
   return BS_OK;
+}
+
+// The request descriptors alone (gather, scatter, decode share this blob).
+int upload_reqs(bs_ctx* c, hipStream_t s, const bs_req_desc* reqs, int n, Slot** out) {
+  return upload(c, s, Key('R', {n}, reqs, sizeof(bs_req_desc) * n),
+                [&](Blob& b) { b.add(reqs, sizeof(bs_req_desc) * n); }, out);
 }
 
 int finish(bs_ctx* c, Slot* sl, hipStream_t s, hipError_t launch, const char* what) {
@@ -160,17 +205,6 @@ int finish(bs_ctx* c, Slot* sl, hipStream_t s, hipError_t launch, const char* wh
   if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord(done)");
   return BS_OK;
 }
-
-// Blob = descriptors followed by an optional work list, 16-byte aligned parts.
-struct Blob {
-  std::vector<unsigned char> bytes;
-  size_t add(const void* p, size_t n) {
-    size_t off = (bytes.size() + 15) & ~size_t(15);
-    bytes.resize(off + n);
-    if (n) std::memcpy(bytes.data() + off, p, n);
-    return off;
-  }
-};
 
 int dtype_bytes(bs_dtype dt) { return dt == BS_F32 ? 4 : (dt == BS_BF16 ? 2 : 0); }
 
@@ -225,42 +259,73 @@ int bs_validate_requests(const bs_req_desc* reqs, int n, int L, int R, int W) {
 }
 
 // ------------------------------------------------------------------ K1
-static int gather_common(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
-                         const void* a_ptr, int64_t stride, int eb, void* b_ptr, bool gather,
-                         int32_t* pos, void* stream) {
+static int gather_common(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int nt,
+                         const void* const* dense, const int64_t* stride, const int* eb, void* const* compact,
+                         bool gather, int32_t* pos, void* stream) {
   if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
   int st = check_reqs(c, reqs, n, L, R, W);
   if (st) return st;
-  if (!(eb == 1 || eb == 2 || eb == 4 || eb == 8 || eb == 16))
-    return fail(c, BS_ERR_UNSUPPORTED, "elem_bytes=%d (supported: 1, 2, 4, 8, 16)", eb);
+  if (nt < 1 || nt > kMaxGather) return fail(c, BS_ERR_INVALID_ARG, "ntensors=%d outside [1, %d]", nt, kMaxGather);
+  if (!dense || !stride || !eb || !compact) return fail(c, BS_ERR_INVALID_ARG, "tensor array is NULL");
+  GatherSet g{};
+  g.count = nt;
+  for (int k = 0; k < nt; ++k) {
+    const int e = eb[k];
+    if (!(e == 1 || e == 2 || e == 4 || e == 8 || e == 16))
+      return fail(c, BS_ERR_UNSUPPORTED, "tensor %d: elem_bytes=%d (supported: 1, 2, 4, 8, 16)", k, e);
+    if (n == 0) continue;
+    if (!dense[k] || !compact[k]) return fail(c, BS_ERR_INVALID_ARG, "tensor %d: pointer is NULL", k);
+    if (stride[k] < (int64_t)W * e)
+      return fail(c, BS_ERR_INVALID_ARG, "tensor %d: row stride %lld < W*elem", k, (long long)stride[k]);
+    if (stride[k] % e || !aligned(dense[k], e) || !aligned(compact[k], e))
+      return fail(c, BS_ERR_INVALID_ARG, "tensor %d: pointers and row stride must be multiples of elem_bytes", k);
+    g.dense[k] = dense[k];
+    g.compact[k] = compact[k];
+    g.stride[k] = stride[k];
+    g.eb[k] = e;
+  }
+  if (pos && !aligned(pos, 4)) return fail(c, BS_ERR_INVALID_ARG, "pos_out must be 4-byte aligned");
   if (n == 0) return BS_OK;
-  if (!a_ptr || !b_ptr) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
-  if (stride < (int64_t)W * eb) return fail(c, BS_ERR_INVALID_ARG, "row stride %lld < W*elem", (long long)stride);
-  if (stride % eb || !aligned(a_ptr, eb) || !aligned(b_ptr, eb) || (pos && !aligned(pos, 4)))
-    return fail(c, BS_ERR_INVALID_ARG, "pointers and row stride must be multiples of elem_bytes");
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  st = upload(c, s, reqs, sizeof(bs_req_desc) * n, &sl);
+  st = upload_reqs(c, s, reqs, n, &sl);
   if (st) return st;
   const bs_req_desc* dreqs = static_cast<const bs_req_desc*>(sl->d);
-  hipError_t e = gather ? launch_gather(dreqs, n, L, a_ptr, stride, eb, b_ptr, pos, s)
-                        : launch_scatter(dreqs, n, L, a_ptr, eb, b_ptr, stride, s);
+  hipError_t e = gather ? launch_gather(dreqs, n, L, g, pos, s) : launch_scatter(dreqs, n, L, g, s);
   return finish(c, sl, s, e, gather ? "gather launch" : "scatter launch");
 }
 
 int bs_gather_active_blocks(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
                             const void* src, int64_t src_row_stride_bytes, int elem_bytes,
                             void* dst, int32_t* pos_out, void* stream) {
-  return gather_common(c, reqs, n, L, R, W, src, src_row_stride_bytes, elem_bytes, dst, true, pos_out, stream);
+  return gather_common(c, reqs, n, L, R, W, 1, &src, &src_row_stride_bytes, &elem_bytes, &dst, true, pos_out, stream);
 }
 
 int bs_scatter_active_blocks(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W,
                              const void* src_compact, int elem_bytes, void* dst_dense,
                              int64_t dst_row_stride_bytes, void* stream) {
-  return gather_common(c, reqs, n, L, R, W, src_compact, dst_row_stride_bytes, elem_bytes, dst_dense, false,
+  const void* dense = dst_dense;
+  void* compact = const_cast<void*>(src_compact);
+  return gather_common(c, reqs, n, L, R, W, 1, &dense, &dst_row_stride_bytes, &elem_bytes, &compact, false,
                        nullptr, stream);
+}
+
+int bs_gather_active_blocks_n(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int ntensors,
+                              const void* const* src, const int64_t* src_row_stride_bytes,
+                              const int* elem_bytes, void* const* dst, int32_t* pos_out, void* stream) {
+  return gather_common(c, reqs, n, L, R, W, ntensors, src, src_row_stride_bytes, elem_bytes, dst, true, pos_out,
+                       stream);
+}
+
+int bs_scatter_active_blocks_n(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int ntensors,
+                               const void* const* src_compact, const int* elem_bytes, void* const* dst_dense,
+                               const int64_t* dst_row_stride_bytes, void* stream) {
+  // the kernel writes through the dense pointers; the set stores them as const
+  return gather_common(c, reqs, n, L, R, W, ntensors, const_cast<const void* const*>(dst_dense),
+                       dst_row_stride_bytes, elem_bytes, const_cast<void* const*>(src_compact), false, nullptr,
+                       stream);
 }
 
 // ------------------------------------------------------------------ K2
@@ -299,49 +364,43 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  Blob blob;
-  const size_t off_reqs = blob.add(reqs, sizeof(bs_req_desc) * n);
-  size_t off_items = 0;
-  int n_items = 0;
-  if (dt == BS_BF16) {
-    std::vector<AttnItem> items;
-    items.reserve((size_t)n * Hkv);
-    for (int i = 0; i < n; ++i) {
-      const int len = reqs[i].p + reqs[i].g;
-      for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, 0, len, 0, 1, 0, 0});
-    }
-    // longest rows first so the tail of the grid is made of short items
-    std::stable_sort(items.begin(), items.end(),
-                     [](const AttnItem& x, const AttnItem& y) { return (x.t1 - x.t0) > (y.t1 - y.t0); });
-    n_items = (int)items.size();
-    off_items = blob.add(items.data(), sizeof(AttnItem) * items.size());
-  }
   Slot* sl = nullptr;
-  st = upload(c, s, blob.bytes.data(), blob.bytes.size(), &sl);
+  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n), [&](Blob& blob) {
+    blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
+    if (dt == BS_BF16) {
+      std::vector<AttnItem> items;
+      items.reserve((size_t)n * Hkv);
+      for (int i = 0; i < n; ++i) {
+        const Geo gq = geo_of(reqs[i], L);
+        for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, 0});
+      }
+      // longest rows first: neighbours in a workgroup have similar lengths and
+      // the tail of the grid is made of short items
+      std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
+      blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * items.size());
+      blob.meta[2] = (int)items.size();
+    }
+  }, &sl);
   if (st) return st;
   const char* base = static_cast<const char*>(sl->d);
   AttnArgs a{};
-  a.reqs = reinterpret_cast<const bs_req_desc*>(base + off_reqs);
-  a.items = reinterpret_cast<const AttnItem*>(base + off_items);
-  a.n_items = n_items;
+  a.reqs = reinterpret_cast<const bs_req_desc*>(base + sl->meta[0]);
+  a.items = reinterpret_cast<const AttnItem*>(base + sl->meta[1]);
+  a.n_items = sl->meta[2];
   a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = G; a.RB = RB; a.R = R; a.W = W;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
   a.scale_log2e = a.scale * 1.4426950408889634f;
   a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
   a.write_back = write_back ? 1 : 0;
-  a.ws_o = nullptr; a.ws_ml = nullptr;
   (void)ws;
-  hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, n, 0, s);
+  hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
   return finish(c, sl, s, e, "attention launch");
 }
 
 // ------------------------------------------------------------------ K3
 size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype dt) {
-  const int eb = dtype_bytes(dt);
-  if (n <= 0 || L <= 0 || V <= 0 || eb == 0) return 0;
-  const int64_t per = kDecChunkBytes / eb;
-  const int64_t nchunk = ((int64_t)V + per - 1) / per;
-  return (size_t)n * L * nchunk * sizeof(DecPartial);
+  if (n <= 0 || L <= 0 || V <= 0 || dtype_bytes(dt) == 0) return 0;
+  return dec_workspace_bytes(n, L, dec_parts(V, dtype_bytes(dt)));
 }
 
 int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
@@ -363,6 +422,8 @@ int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
   if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)logits_dt);
   if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
   if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
+  if ((int64_t)n * L * dec_parts(V, dtype_bytes(logits_dt)) > INT32_MAX)
+    return fail(c, BS_ERR_UNSUPPORTED, "n * L * row parts exceeds the launch grid");
   if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
   if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
   if (logits_row_stride < V || (logits_row_stride * eb) % 16)
@@ -380,15 +441,15 @@ int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  int st = upload(c, s, reqs, sizeof(bs_req_desc) * n, &sl);
+  int st = upload_reqs(c, s, reqs, n, &sl);
   if (st) return st;
   DecArgs a{};
   a.reqs = static_cast<const bs_req_desc*>(sl->d);
   a.n = n; a.L = L; a.V = V;
-  a.nchunk = (int)(((int64_t)V + kDecChunkBytes / eb - 1) / (kDecChunkBytes / eb));
   a.logits = logits; a.row_stride = logits_row_stride;
   a.tokens = tokens; a.masked = masked; a.tau = tau; a.q_min = q_min; a.eos_id = eos_id;
   a.n_unmasked = n_unmasked; a.done = done; a.eos_seen = eos_seen; a.conf_out = conf_out;
+  a.parts = dec_parts(V, dtype_bytes(logits_dt));
   a.part = static_cast<DecPartial*>(ws);
   hipError_t e = launch_decode(a, logits_dt, s);
   return finish(c, sl, s, e, "decode launch");
@@ -457,26 +518,27 @@ int bs_kv_scatter_compact(bs_ctx* c, const bs_copy_seg* segs, int nseg, int n_la
     }
   }
   if (nseg == 0 || n_layers == 0 || total_chunks == 0) return BS_OK;
-  std::vector<CopyUnit> units;
-  units.reserve((size_t)total_chunks);
-  for (int i = 0; i < nseg; ++i) {
-    const int64_t nc = (segs[i].len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
-    for (int64_t k = 0; k < nc; ++k) units.push_back(CopyUnit{i, (int32_t)k});
-  }
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  Blob blob;
-  const size_t off_segs = blob.add(segs, sizeof(bs_copy_seg) * nseg);
-  const size_t off_units = blob.add(units.data(), sizeof(CopyUnit) * units.size());
   Slot* sl = nullptr;
-  int st = upload(c, s, blob.bytes.data(), blob.bytes.size(), &sl);
+  int st = upload(c, s, Key('C', {nseg, row_bytes}, segs, sizeof(bs_copy_seg) * nseg), [&](Blob& blob) {
+    std::vector<CopyUnit> units;
+    units.reserve((size_t)total_chunks);
+    for (int i = 0; i < nseg; ++i) {
+      const int64_t nc = (segs[i].len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
+      for (int64_t k = 0; k < nc; ++k) units.push_back(CopyUnit{i, (int32_t)k});
+    }
+    blob.meta[0] = (int)blob.add(segs, sizeof(bs_copy_seg) * nseg);
+    blob.meta[1] = (int)blob.add(units.data(), sizeof(CopyUnit) * units.size());
+    blob.meta[2] = (int)units.size();
+  }, &sl);
   if (st) return st;
   const char* base = static_cast<const char*>(sl->d);
   CopyArgs a{};
-  a.segs = reinterpret_cast<const bs_copy_seg*>(base + off_segs);
-  a.units = reinterpret_cast<const CopyUnit*>(base + off_units);
-  a.n_units = (int)units.size();
+  a.segs = reinterpret_cast<const bs_copy_seg*>(base + sl->meta[0]);
+  a.units = reinterpret_cast<const CopyUnit*>(base + sl->meta[1]);
+  a.n_units = sl->meta[2];
   a.n_layers = n_layers; a.Hkv = Hkv; a.row_bytes = row_bytes;
   a.src_k = static_cast<const char*>(src_k); a.src_v = static_cast<const char*>(src_v);
   a.src_ls = src_layer_stride; a.W_src = W_src;

@@ -121,73 +121,149 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a, int jblocks) {
 }
 
 // ------------------------------------------------------------------ bf16 MFMA
-// A workgroup serves one (request, KV head). Its waves form S key-split
-// groups of GW = G * RB waves: the waves of a group share one K/V tile in LDS
-// (one wave per query head of the group and 32-row block), and group s takes
-// tiles s, s + S, ... of the request's key range. After the loop the groups'
-// (max, sum, O) partials are merged through LDS, so splitting a row never
-// costs HBM traffic.
-template <int D, int KT, int S, int GTMIN>
-struct TileCfg {
-  static constexpr int KS = D + 8;                  // K tile row stride (elements), 16-byte rows
-  static constexpr int VS = KT + 4;                 // V^T row stride (elements), 8-byte aligned
-  static constexpr int KCH = KT * D / 8;            // 16-byte chunks of a K tile
-  static constexpr int VBLK = (KT / 8) * (D / 8);   // 8x8 blocks of a V tile
-  static constexpr int MAXK = (KCH + GTMIN - 1) / GTMIN;
-  static constexpr int MAXV = (VBLK + GTMIN - 1) / GTMIN;
-  static constexpr int TILE_ELEMS = KT * KS + D * VS;
-};
+// Tiles move HBM -> LDS by direct DMA (global_load_lds_dwordx4: lane l of a
+// wave instruction fills bytes [16 l, 16 l + 16) of a 1 KiB LDS block), through
+// a ring of NS stages per group, so loads occupy no registers and NS - 1 tiles
+// stay in flight while one is consumed. Rows are stored with their 16-byte
+// chunks XOR-swizzled (slot = chunk ^ swz(row)); the permutation is applied on
+// the global side, since each lane picks which chunk it fetches. K is read as
+// the MFMA A operand with one 16-byte LDS read; V is read with the LDS
+// transpose load (ds_read_b64_tr_b16), which hands each lane 4 consecutive keys
+// of one feature: two of them form the 8-key A operand of O^T += V^T P^T.
+// The DMA is issued through inline assembly and waited for with explicit
+// vmcnt counts: the compiler's waitcnt pass cannot see it, and would otherwise
+// drain every stage in flight before reading the current one.
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
-template <int D, int KT, int S, int GTMIN, int MAXT, int MINW>
-__global__ __launch_bounds__(MAXT, MINW) void k_attn_bf16(AttnArgs a) {
-  using C = TileCfg<D, KT, S, GTMIN>;
+// XOR swizzle of a row's 16-byte slots. Rows r0..r0+3 (r0 % 4 == 0) differ in
+// bits 1..2, so the transpose reads of 4 consecutive keys x 2 chunks hit 8
+// distinct slots; any 16 consecutive rows get distinct slots for one chunk.
+template <int NCH>
+__device__ inline int swz(int row) {
+  const int base = ((row & 3) << 1) | ((row >> 2) & 1);
+  return NCH == 16 ? (base | (row & 8)) : base;
+}
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)p));
+}
+
+// One wave instruction: 64 lanes x 16 bytes, HBM -> LDS block at `lds` (wave-uniform).
+__device__ inline void dma16(uint32_t lds, const void* gptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(gptr)
+               : "memory");
+}
+__device__ inline uint64_t uniform64(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+// Same, addressed as a wave-uniform base (SGPRs) plus a 32-bit per-lane byte offset.
+__device__ inline void dma16_sv(uint32_t lds, uint64_t base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(off), "s"(uniform64(reinterpret_cast<const void*>(base)))
+               : "memory");
+}
+
+// Wait until at most n of this wave's vector-memory operations are outstanding.
+__device__ inline void wait_vm(int n) {
+  // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+#define BS_VM(N) case N: __builtin_amdgcn_s_waitcnt(((N) & 15) | (((N) >> 4) << 14) | (7 << 4) | (15 << 8)); break;
+  switch (n) {
+    BS_VM(0) BS_VM(1) BS_VM(2) BS_VM(3) BS_VM(4) BS_VM(5) BS_VM(6) BS_VM(7) BS_VM(8) BS_VM(9) BS_VM(10)
+    BS_VM(11) BS_VM(12) BS_VM(13) BS_VM(14) BS_VM(15) BS_VM(16) BS_VM(17) BS_VM(18) BS_VM(19) BS_VM(20)
+    BS_VM(21) BS_VM(22) BS_VM(23) BS_VM(24) BS_VM(25) BS_VM(26) BS_VM(27) BS_VM(28) BS_VM(29) BS_VM(30)
+    BS_VM(31) BS_VM(32)
+    default: __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); break;
+  }
+#undef BS_VM
+}
+
+// One (request, KV head) item processed by GW waves that share its K/V tiles:
+// wave wg of the group serves query head c * G + wg / RB and rows
+// 32 * (wg % RB) .. + 32 of the block. SHARED = false is the single-wave case
+// (GW = 1): the wave owns its ring, so no barrier is needed anywhere.
+template <int D, int KT, int NS, bool SHARED, int MAXBLK>
+__device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t* ring, int GW, int wg,
+                                 int lane) {
   constexpr int NKK = D / 16;
   constexpr int NDT = D / 32;
-  // tiles during the loop; the split groups' partials after it
-  constexpr int MERGE_FLOATS = (S - 1) * ((MAXT / 64) / S) * 64 * (2 + NDT * 16);
-  constexpr int TILE_BYTES = S * C::TILE_ELEMS * 2;
-  constexpr int LDS_BYTES = TILE_BYTES > MERGE_FLOATS * 4 ? TILE_BYTES : MERGE_FLOATS * 4;
-  __shared__ __align__(16) uint16_t lds[LDS_BYTES / 2];
-
-  const AttnItem it = a.items[blockIdx.x];
-  const bs_req_desc r = a.reqs[it.req];
-  const Geo q = geo_of(r, a.L);
-  const int GW = a.G * a.RB;                       // waves per split group
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 5, n = lane & 31;
-  const int grp = w / GW, wg = w - grp * GW;
-  const int gth = GW * 64, gt = tid - grp * gth;   // threads of this group, index within it
+  constexpr int NCH = D / 8;                      // 16-byte chunks per row
+  constexpr int RPB = 64 / NCH;                   // rows per 1 KiB DMA block
+  constexpr int BPT = KT / RPB;                   // blocks per K (or V) tile
+  constexpr int TILE = KT * D;                    // elements of one K (or V) tile
+  constexpr int STAGE = 2 * TILE;                 // K tile then V tile
+  const int g = lane >> 5, n = lane & 31;
   const int c = it.kvh;
   const int h = c * a.G + wg / a.RB;
   const int j = (wg % a.RB) * 32 + n;
-  const int bs = q.s, be = q.s + q.B;
-  uint16_t* ks = lds + grp * C::TILE_ELEMS;
-  uint16_t* vt = ks + KT * C::KS;
+  const int bs = it.s, be = it.s + it.B, len = it.len;
 
-  const int64_t cache_off = (((int64_t)r.row * a.Hkv + c) * a.W + r.off) * D;
+  const int64_t cache_off = (((int64_t)it.row * a.Hkv + c) * a.W + it.off) * D;
   const uint16_t* kcb = static_cast<const uint16_t*>(a.k_cache) + cache_off;
   const uint16_t* vcb = static_cast<const uint16_t*>(a.v_cache) + cache_off;
-  uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
-  uint16_t* vcw = static_cast<uint16_t*>(a.v_cache) + cache_off;
   const int64_t fstride = (int64_t)a.Hkv * D;
   const uint16_t* knb = static_cast<const uint16_t*>(a.k_new) + ((int64_t)it.req * a.L * a.Hkv + c) * D;
   const uint16_t* vnb = static_cast<const uint16_t*>(a.v_new) + ((int64_t)it.req * a.L * a.Hkv + c) * D;
-  // source of logical key t (clamped into the row; rows past the range are masked later)
-  auto krow = [&](int t) -> const uint16_t* {
-    t = min(t, it.t1 - 1);
-    const bool fresh = (t >= bs) & (t < be);
-    return fresh ? knb + (int64_t)(t - bs) * fstride : kcb + (int64_t)t * D;
+
+  // DMA work of this wave per stage: blocks wg, wg + GW, ... of the 2 * BPT.
+  // Block bi covers rows [rb * RPB, rb * RPB + RPB) of tensor bi / BPT; lane l
+  // fills slot l % NCH of row rb * RPB + l / NCH with global chunk slot ^ swz(row).
+  const int nblk = (2 * BPT - wg + GW - 1) / GW;
+  const int drow = lane / NCH, dslot = lane % NCH;
+  uint32_t doff[MAXBLK];                          // byte offset of this lane's chunk within a tile
+#pragma unroll
+  for (int k = 0; k < MAXBLK; ++k) {
+    const int bi = min(wg + k * GW, 2 * BPT - 1);
+    const int row = (bi % BPT) * RPB + drow;
+    doff[k] = (uint32_t)(row * D + ((dslot ^ swz<NCH>(row)) * 8)) * 2u;
+  }
+  const uint32_t ring_lds = lds_addr(ring);
+  auto issue = [&](int stage, int tb) {
+    const uint32_t sbase = __builtin_amdgcn_readfirstlane(ring_lds + (uint32_t)(stage * STAGE * 2));
+    if (tb + KT <= len && (tb + KT <= bs || tb >= be)) {
+      // whole tile inside the cached part of the row: uniform base + lane offset
+      const uint64_t kb = uniform64(kcb + (int64_t)tb * D), vb = uniform64(vcb + (int64_t)tb * D);
+#pragma unroll
+      for (int k = 0; k < MAXBLK; ++k) {
+        if (k < nblk) {
+          const int bi = wg + k * GW;
+          const int tensor = bi / BPT, rb = bi - tensor * BPT;
+          dma16_sv(sbase + (uint32_t)((tensor * TILE + rb * RPB * D) * 2), tensor ? vb : kb, doff[k]);
+        }
+      }
+    } else {
+      // tile holds fresh block rows or runs past the row end: per-lane sources
+      for (int k = 0; k < nblk; ++k) {
+        const int bi = wg + k * GW;
+        const int tensor = bi / BPT, rb = bi - tensor * BPT;
+        const int row = rb * RPB + drow;
+        const int t = min(tb + row, len - 1);        // rows past the end repeat a valid key (masked later)
+        const bool fresh = (t >= bs) & (t < be);
+        const uint16_t* src = tensor ? (fresh ? vnb + (int64_t)(t - bs) * fstride : vcb + (int64_t)t * D)
+                                     : (fresh ? knb + (int64_t)(t - bs) * fstride : kcb + (int64_t)t * D);
+        const int chunk = dslot ^ swz<NCH>(row);
+        dma16(sbase + (uint32_t)((tensor * TILE + rb * RPB * D) * 2), src + chunk * 8);
+      }
+    }
   };
-  auto vrow = [&](int t) -> const uint16_t* {
-    t = min(t, it.t1 - 1);
-    const bool fresh = (t >= bs) & (t < be);
-    return fresh ? vnb + (int64_t)(t - bs) * fstride : vcb + (int64_t)t * D;
-  };
+
+  const int ntiles = (len + KT - 1) / KT;
+  // prologue: stages 0 .. NS-2 (issued before anything else so the first
+  // tiles are in flight while the queries load)
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < ntiles) issue(st, st * KT);
 
   // queries of this lane's column as MFMA B operands: feature d = 16 kk + 8 g + e
   bf16x8_t qb[NKK];
   {
-    const bool qv = j < q.B;
-    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + (((int64_t)it.req * a.L + min(j, q.B - 1)) * a.Hq + h) * D;
+    const bool qv = j < it.B;
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + (((int64_t)it.req * a.L + min(j, it.B - 1)) * a.Hq + h) * D;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       v4u t = ld16(qp + 16 * kk + 8 * g);
@@ -195,54 +271,23 @@ __global__ __launch_bounds__(MAXT, MINW) void k_attn_bf16(AttnArgs a) {
       qb[kk] = __builtin_bit_cast(bf16x8_t, t);
     }
   }
-
-  v4u kreg[C::MAXK];
-  v4u vreg[C::MAXV * 8];
-  auto load_tile = [&](int tb) {
+  // loop-invariant parts of this lane's LDS read addresses (elements)
+  int koff[NKK];
 #pragma unroll
-    for (int k = 0; k < C::MAXK; ++k) {
-      const int cid = min(gt + k * gth, C::KCH - 1);
-      kreg[k] = ld16(krow(tb + cid / (D / 8)) + (cid % (D / 8)) * 8);
-    }
+  for (int kk = 0; kk < NKK; ++kk) koff[kk] = n * D + (((2 * kk + g) ^ swz<NCH>(n)) * 8);
+  const int q16 = lane >> 4, j16 = lane & 15;
+  const int vrow = 4 * (q16 >> 1) + (j16 >> 2);              // + sub*32 + 16 ks + 8 h2
+  int voff[NDT][2][2];
 #pragma unroll
-    for (int k = 0; k < C::MAXV; ++k) {
-      const int bid = min(gt + k * gth, C::VBLK - 1);
-      const int kg = bid / (D / 8), dc = bid % (D / 8);
+  for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vreg[k * 8 + e] = ld16(vrow(tb + kg * 8 + e) + dc * 8);
-    }
-  };
-  // registers -> LDS (K as is, V transposed in 8x8 blocks)
-  auto store_tile = [&](int tb) {
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-    for (int k = 0; k < C::MAXK; ++k) {
-      const int cid = gt + k * gth;
-      if (cid < C::KCH) {
-        const int tt = cid / (D / 8), dc = cid % (D / 8);
-        st16(&ks[tt * C::KS + dc * 8], kreg[k]);
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int row = 16 * ks + 8 * h2 + vrow;                // row within a 32-key sub-tile
+        const int col = 32 * dt + 16 * (q16 & 1) + 4 * (j16 & 3);
+        voff[dt][ks][h2] = row * D + (((col >> 3) ^ swz<NCH>(row)) * 8) + (col & 7);
       }
-    }
-#pragma unroll
-    for (int k = 0; k < C::MAXV; ++k) {
-      const int bid = gt + k * gth;
-      if (bid < C::VBLK) {
-        const int kg = bid / (D / 8), dc = bid % (D / 8);
-#pragma unroll
-        for (int dd = 0; dd < 8; ++dd) {
-          uint32_t o4[4];
-#pragma unroll
-          for (int qi = 0; qi < 4; ++qi) {
-            const uint32_t lo = vreg[k * 8 + 2 * qi][dd >> 1];
-            const uint32_t hi = vreg[k * 8 + 2 * qi + 1][dd >> 1];
-            o4[qi] = (dd & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-          }
-          uint2* dst = reinterpret_cast<uint2*>(&vt[(dc * 8 + dd) * C::VS + kg * 8]);
-          dst[0] = make_uint2(o4[0], o4[1]);
-          dst[1] = make_uint2(o4[2], o4[3]);
-        }
-      }
-    }
-  };
 
   f32x16_t o[NDT];
 #pragma unroll
@@ -250,136 +295,109 @@ __global__ __launch_bounds__(MAXT, MINW) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) o[dt][rr] = 0.0f;
   float mrun = -__builtin_inff(), lsum = 0.0f;
-  const int ntiles = (it.t1 - it.t0 + KT - 1) / KT;
-  const int rounds = (ntiles + S - 1) / S;   // identical for every group: barriers stay uniform
-  if (grp < ntiles) load_tile(it.t0 + grp * KT);
-  for (int rd = 0; rd < rounds; ++rd) {
-    const int tile = rd * S + grp;
-    const bool active = tile < ntiles;
-    const int tb = it.t0 + tile * KT;
-    __syncthreads();
-    if (active) store_tile(tb);
-    __syncthreads();
-    if (tile + S < ntiles) load_tile(tb + S * KT);
-    if (active) {
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const int nxt = tile + NS - 1;
+    if (nxt < ntiles) issue(nxt % NS, nxt * KT);
+    // this tile's stage has landed once only the later stages' DMAs remain
+    wait_vm(nblk * (min(ntiles, tile + NS) - tile - 1));
+    if constexpr (SHARED) __syncthreads();
+    const uint16_t* kt = ring + (tile % NS) * STAGE;
+    const uint16_t* vtl = kt + TILE;
+    const int tb = tile * KT;
 #pragma unroll
-      for (int sub = 0; sub < KT / 32; ++sub) {
-        const int sb = tb + sub * 32;
-        if (sb >= it.t1) break;
-        f32x16_t sacc;
+    for (int sub = 0; sub < KT / 32; ++sub) {
+      const int sb = tb + sub * 32;
+      if (sb >= len) break;
+      f32x16_t sacc;
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) sacc[rr] = 0.0f;
+      for (int rr = 0; rr < 16; ++rr) sacc[rr] = 0.0f;
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-          const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&ks[(sub * 32 + n) * C::KS + 16 * kk + 8 * g]);
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[kk], sacc, 0, 0, 0);
-        }
-        // lane (g, n) holds S^T[key 8 (rr / 4) + 4 g + rr % 4][query n]
-        float mx = -__builtin_inff();
+      for (int kk = 0; kk < NKK; ++kk) {
+        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kt + sub * 32 * D + koff[kk]);
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[kk], sacc, 0, 0, 0);
+      }
+      // lane (g, n) holds S^T[key 8 (rr / 4) + 4 g + rr % 4][query n] (unscaled)
+      if (sb + 32 > len) {                       // ragged last sub-tile only
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int key = sb + 8 * (rr >> 2) + 4 * g + (rr & 3);
-          sacc[rr] = key < it.t1 ? sacc[rr] * a.scale_log2e : -__builtin_inff();
-          mx = fmaxf(mx, sacc[rr]);
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        for (int rr = 0; rr < 16; ++rr)
+          if (sb + 8 * (rr >> 2) + 4 * g + (rr & 3) >= len) sacc[rr] = -__builtin_inff();
+      }
+      float mx = sacc[0];
+#pragma unroll
+      for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, sacc[rr]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
+      // lazy rescale: keep the reference max until a score exceeds it by 2^8,
+      // so the O accumulators are rescaled a handful of times per row
+      if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {
         const float mnew = fmaxf(mrun, mx);
         const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
-        bf16x8_t pb0, pb1;
-        float ps = 0.0f;
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const float p = __builtin_amdgcn_exp2f(sacc[rr] - mnew);
-          ps += p;
-          if (rr < 8)
-            pb0[rr] = (__bf16)p;
-          else
-            pb1[rr - 8] = (__bf16)p;
-        }
-        lsum = lsum * alpha + ps;
-        mrun = mnew;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-          for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
-#pragma unroll
-          for (int kst = 0; kst < 2; ++kst) {
-            const uint16_t* vp = &vt[(dt * 32 + n) * C::VS + sub * 32 + 16 * kst + 4 * g];
-            typedef uint32_t v2u __attribute__((ext_vector_type(2)));
-            const v2u lo = *reinterpret_cast<const v2u*>(vp);
-            const v2u hi = *reinterpret_cast<const v2u*>(vp + 8);
-            const bf16x8_t va = __builtin_bit_cast(bf16x8_t, v4u{lo.x, lo.y, hi.x, hi.y});
-            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, kst ? pb1 : pb0, o[dt], 0, 0, 0);
-          }
-        }
-      }
-    }
-  }
-  float lt = lsum + __shfl_xor(lsum, 32, 64);
-  if constexpr (S > 1) {
-    // merge the key-split groups: groups 1..S-1 park (m, l, O) in LDS
-    float* mb = reinterpret_cast<float*>(lds);                  // [S-1][GW][64][2]
-    float* ob = mb + (S - 1) * GW * 64 * 2;                     // [S-1][GW][NDT*16][64]
-    __syncthreads();
-    if (grp > 0) {
-      const int slot = (grp - 1) * GW + wg;
-      mb[(slot * 64 + lane) * 2 + 0] = mrun;
-      mb[(slot * 64 + lane) * 2 + 1] = lt;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) ob[((int64_t)slot * NDT * 16 + dt * 16 + rr) * 64 + lane] = o[dt][rr];
-    }
-    __syncthreads();
-    if (grp == 0) {
-      float M = mrun;
-#pragma unroll
-      for (int s2 = 1; s2 < S; ++s2) M = fmaxf(M, mb[(((s2 - 1) * GW + wg) * 64 + lane) * 2]);
-      const float f0 = __builtin_amdgcn_exp2f(mrun - M);
-      lt *= f0;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= f0;
-#pragma unroll
-      for (int s2 = 1; s2 < S; ++s2) {
-        const int slot = (s2 - 1) * GW + wg;
-        const float fs = __builtin_amdgcn_exp2f(mb[(slot * 64 + lane) * 2] - M);
-        lt += mb[(slot * 64 + lane) * 2 + 1] * fs;
+        lsum *= alpha;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-          for (int rr = 0; rr < 16; ++rr) o[dt][rr] += ob[((int64_t)slot * NDT * 16 + dt * 16 + rr) * 64 + lane] * fs;
+          for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
+        mrun = mnew;
       }
+      bf16x8_t pb0, pb1;
+      const float nm = -mrun;
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[rr], a.scale_log2e, nm));
+        lsum += p;
+        if (rr < 8)
+          pb0[rr] = (__bf16)p;
+        else
+          pb1[rr - 8] = (__bf16)p;
+      }
+      const uint16_t* vs = vtl + sub * 32 * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
+          const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
+          const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ks ? pb1 : pb0, o[dt], 0, 0, 0);
+        }
     }
+    // the stage is refilled NS - 1 tiles later: every reader must be done
+    // (a single wave consumed its LDS reads through the MFMAs above)
+    if constexpr (SHARED) __syncthreads();
   }
-  // in-place KV update: the fresh block rows of this KV head go to the cache
-  // slot [off + s, off + s + B) (the item whose key range holds the block)
-  if (a.write_back && it.t0 <= bs && bs < it.t1) {
-    constexpr int MAXWB = (64 * D / 8 + MAXT / 2 - 1) / (MAXT / 2);
-    const int nth = blockDim.x, nch = q.B * (D / 8);
-    v4u kw[MAXWB], vw[MAXWB];
+  const float lt = lsum + __shfl_xor(lsum, 32, 64);
+  // in-place KV update: the group's waves store the fresh block rows of this
+  // KV head into the cache slot [off + s, off + s + B)
+  if (a.write_back) {
+    constexpr int MAXWB = 32 * D / 8 / 64;          // per wave, for a 32-row block
+    uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
+    uint16_t* vcw = static_cast<uint16_t*>(a.v_cache) + cache_off;
+    const int nch = it.B * (D / 8);
+    const int gt = wg * 64 + lane, gth = GW * 64;
+    for (int base = 0; base < nch; base += gth * MAXWB) {
+      v4u kw[MAXWB], vw[MAXWB];
 #pragma unroll
-    for (int u = 0; u < MAXWB; ++u) {
-      const int cid = min(tid + u * nth, nch - 1);
-      const int64_t src = (int64_t)(cid / (D / 8)) * fstride + (cid % (D / 8)) * 8;
-      kw[u] = ld16(knb + src);
-      vw[u] = ld16(vnb + src);
-    }
+      for (int u = 0; u < MAXWB; ++u) {
+        const int cid = min(base + gt + u * gth, nch - 1);
+        const int64_t src = (int64_t)(cid / (D / 8)) * fstride + (cid % (D / 8)) * 8;
+        kw[u] = ld16(knb + src);
+        vw[u] = ld16(vnb + src);
+      }
 #pragma unroll
-    for (int u = 0; u < MAXWB; ++u) {
-      const int cid = tid + u * nth;
-      if (cid < nch) {
-        const int64_t dst = (int64_t)(bs + cid / (D / 8)) * D + (cid % (D / 8)) * 8;
-        st16(kcw + dst, kw[u]);
-        st16(vcw + dst, vw[u]);
+      for (int u = 0; u < MAXWB; ++u) {
+        const int cid = base + gt + u * gth;
+        if (cid < nch) {
+          const int64_t dst = (int64_t)(bs + cid / (D / 8)) * D + (cid % (D / 8)) * 8;
+          st16(kcw + dst, kw[u]);
+          st16(vcw + dst, vw[u]);
+        }
       }
     }
   }
   // lane (g, n): O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4][query n]
-  if (grp == 0 && j < a.L) {
-    const float inv = (j < q.B) ? 1.0f / lt : 0.0f;
+  if (j < a.L) {
+    const float inv = (j < it.B) ? 1.0f / lt : 0.0f;
     uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)it.req * a.L + j) * a.Hq + h) * D;
+    typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -390,25 +408,46 @@ __global__ __launch_bounds__(MAXT, MINW) void k_attn_bf16(AttnArgs a) {
         const __bf16 b3 = (__bf16)(o[dt][4 * rq + 3] * inv);
         const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
         const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) | ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
-        *reinterpret_cast<uint2*>(op + dt * 32 + 8 * rq + 4 * g) = make_uint2(w0, w1);
+        *reinterpret_cast<v2u*>(op + dt * 32 + 8 * rq + 4 * g) = v2u{w0, w1};
       }
   }
 }
 
-// Launch shapes: GW = G * ceil(L / 32) waves share a tile; MHA (GW = 1) splits
-// each row four ways inside the workgroup, GW 2..4 two ways, GW 5..8 not at all.
-int attn_splits(int GW) { return GW == 1 ? 4 : (GW <= 4 ? 2 : 1); }
+// One query head per KV head and at most 32 block rows (MHA with L <= 32):
+// four independent waves per workgroup, each owning one item and an NS-stage
+// ring of 32-key tiles.
+template <int D, int NS>
+__global__ __launch_bounds__(256, 1) void k_attn_bf16_wave(AttnArgs a) {
+  constexpr int STAGE = 2 * 32 * D;
+  __shared__ __align__(1024) uint16_t lds[4 * NS * STAGE];
+  // the wave index is wave-uniform: through readfirstlane every quantity
+  // derived from it (item, DMA block, base pointers) lives in SGPRs
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int idx = blockIdx.x * 4 + w;
+  if (idx >= a.n_items) return;
+  attn_item<D, 32, NS, false, 2 * (32 * D / 512)>(a, a.items[idx], lds + w * NS * STAGE, 1, 0, threadIdx.x & 63);
+}
+
+// GW = G * ceil(L / 32) >= 2 waves share each item's 64-key tiles.
+template <int D, int NS, int GWMIN>
+__global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
+  constexpr int STAGE = 2 * 64 * D;
+  constexpr int BLK = 2 * (64 * D / 512);         // DMA blocks per stage
+  __shared__ __align__(1024) uint16_t lds[NS * STAGE];
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  attn_item<D, 64, NS, true, (BLK + GWMIN - 1) / GWMIN>(a, a.items[blockIdx.x], lds, blockDim.x >> 6, w,
+                                                         threadIdx.x & 63);
+}
 
 template <int D>
 hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
-  const int S = attn_splits(GW);
-  const dim3 grid(a.n_items), block(64 * GW * S);
-  if (S == 4)
-    hipLaunchKernelGGL((k_attn_bf16<D, 32, 4, 64, 256, 1>), grid, block, 0, s, a);
-  else if (S == 2)
-    hipLaunchKernelGGL((k_attn_bf16<D, 32, 2, 128, 512, 1>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((k_attn_bf16<D, 64, 1, 320, 512, 1>), grid, block, 0, s, a);
+  if (GW == 1) {
+    hipLaunchKernelGGL((k_attn_bf16_wave<D, 2>), dim3((a.n_items + 3) / 4), dim3(256), 0, s, a);
+  } else if (GW <= 4) {
+    hipLaunchKernelGGL((k_attn_bf16_group<D, 3, 2>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_attn_bf16_group<D, 3, 5>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -421,9 +460,7 @@ hipError_t launch_attn_f32(const AttnArgs& a, int n_req, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bf16(const AttnArgs& a, int n_req, int n_slots, hipStream_t s) {
-  (void)n_req;
-  (void)n_slots;
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
   const int GW = a.G * a.RB;
   if (a.D == 128) return launch_bf16_d<128>(a, GW, s);
   if (a.D == 64) return launch_bf16_d<64>(a, GW, s);

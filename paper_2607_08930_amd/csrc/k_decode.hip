@@ -1,14 +1,18 @@
 // K3: confidence-aware parallel decode (paragraph "Vectorized mixed-schedule
 // execution"; greedy decoding, "Implementation details").
 //
-// Pass 1 (k_decode_rows): one 256-thread workgroup per (masked row, 64 KiB
-// chunk of the vocabulary). Every thread issues all 16 of its 16-byte loads
-// up front, then reduces in registers: chunk max, then sum exp(x - max), then
-// the smallest index attaining the max. Rows that are not masked, and rows past
-// the request's block, exit before reading anything.
-// Pass 2 (k_decode_select): one wave per request; lane j merges row j's chunk
-// partials in chunk order (deterministic), derives the confidence, and the wave
-// ranks the masked positions to apply the threshold/quota rule in place.
+// Two launches. k_decode_parts: a masked row is split into parts of
+// kDecPartChunks chunks of 32 KiB and one 256-thread workgroup streams one
+// part (rows that are not masked exit at once). Within a part the chunks are
+// register double buffered: the next chunk's eight 16-byte loads per thread
+// are in flight while the current one is reduced. Each thread keeps an online
+// (max, sum of exp(x - max)) and the first vector holding its max; the
+// workgroup merges the threads' results, and only threads holding the part max
+// re-read that one vector to find the smallest index attaining it. The part
+// result (max, sum, argmax) goes to the workspace.
+// k_decode_select: one wave per request merges every row's parts and runs the
+// selection. The launch boundary orders the two, so no workgroup waits on
+// another and no cache maintenance is needed inside either kernel.
 #include <float.h>
 #include <limits.h>
 
@@ -18,8 +22,7 @@ namespace bs {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kVecBytes = 16;
-constexpr int kLoads = kDecChunkBytes / (kThreads * kVecBytes);  // 16
+constexpr int kLoads = kDecChunkBytes / (kThreads * 16);  // 8
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ inline float wave_max(float v) {
@@ -62,103 +65,83 @@ struct Lanes<float> {
   __device__ static inline void mask(v4u& v, int e, bool drop) { v[e] = drop ? 0xFF800000u : v[e]; }
 };
 
+// Loads of one chunk: vector u of thread tid starts at element v0 + (u*256 + tid)*N.
+// A vector that starts past the row end re-reads the chunk's first vector (a
+// valid address); elements at or past V are masked when the chunk is folded.
+// A vector starting before V stays inside the row's padded 16-byte stride.
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_decode_rows(DecArgs a) {
+__device__ inline void load_chunk(v4u (&buf)[kLoads], const T* x, int v0, int V, int tid) {
   constexpr int N = Lanes<T>::N;
-  constexpr int CH = kDecChunkBytes / sizeof(T);
-  const int c = blockIdx.x % a.nchunk;
-  const int row = blockIdx.x / a.nchunk;
-  const int i = row / a.L, j = row - i * a.L;
-  const Geo q = geo_of(a.reqs[i], a.L);
-  if (j >= q.B || a.masked[row] == 0) return;
-  const T* x = static_cast<const T*>(a.logits) + (int64_t)row * a.row_stride;
-  const int v0 = c * CH;
-  const int v1 = min(a.V, v0 + CH);
-  const int tid = threadIdx.x;
-
-  // Branch-free loads: a vector that starts past the row end re-reads the
-  // chunk's first vector; elements at or past V are then set to -inf. A vector
-  // that starts before V stays inside the row's padded stride.
-  v4u buf[kLoads];
 #pragma unroll
   for (int u = 0; u < kLoads; ++u) {
     const int e = v0 + (u * kThreads + tid) * N;
-    buf[u] = ld16(x + (e < v1 ? e : v0));
+    buf[u] = ld16(x + (e < V ? e : v0));
   }
-  if (v0 + CH > a.V) {  // last chunk of the row: mask the ragged end
+}
+
+template <typename T>
+__device__ inline void mask_tail(v4u (&buf)[kLoads], int v0, int V, int tid) {
+  constexpr int N = Lanes<T>::N;
+  constexpr int CH = kDecChunkBytes / sizeof(T);
+  if (v0 + CH > V) {  // last chunk of the row only
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
       const int e = v0 + (u * kThreads + tid) * N;
 #pragma unroll
-      for (int k = 0; k < N; ++k) Lanes<T>::mask(buf[u], k, e + k >= v1);
+      for (int k = 0; k < N; ++k) Lanes<T>::mask(buf[u], k, e + k >= V);
     }
-  }
-  // chunk max
-  float m = -__builtin_inff();
-#pragma unroll
-  for (int u = 0; u < kLoads; ++u)
-#pragma unroll
-    for (int e = 0; e < N; ++e) m = fmaxf(m, Lanes<T>::get(buf[u], e));
-  __shared__ float sm[kThreads / 64];
-  __shared__ float ss[kThreads / 64];
-  __shared__ int sa[kThreads / 64];
-  const int w = tid >> 6, lane = tid & 63;
-  float wm = wave_max(m);
-  if (lane == 0) sm[w] = wm;
-  __syncthreads();
-  float M = sm[0];
-#pragma unroll
-  for (int k = 1; k < kThreads / 64; ++k) M = fmaxf(M, sm[k]);
-  // sum of exp(x - M) with independent partial sums per vector lane
-  const float mb = M * kLog2e;
-  float acc[N];
-#pragma unroll
-  for (int e = 0; e < N; ++e) acc[e] = 0.0f;
-#pragma unroll
-  for (int u = 0; u < kLoads; ++u)
-#pragma unroll
-    for (int e = 0; e < N; ++e) acc[e] += __builtin_amdgcn_exp2f(fmaf(Lanes<T>::get(buf[u], e), kLog2e, -mb));
-  float s = 0.0f;
-#pragma unroll
-  for (int e = 0; e < N; ++e) s += acc[e];
-  // smallest index holding M (only threads whose own max is M scan)
-  int arg = INT_MAX;
-  if (m == M) {
-#pragma unroll
-    for (int u = 0; u < kLoads; ++u)
-#pragma unroll
-      for (int e = 0; e < N; ++e) {
-        const int idx = v0 + (u * kThreads + tid) * N + e;
-        if (Lanes<T>::get(buf[u], e) == M && idx < arg) arg = idx;
-      }
-  }
-  float ws_ = wave_sum(s);
-  int wa = wave_min_i(arg);
-  if (lane == 0) {
-    ss[w] = ws_;
-    sa[w] = wa;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    float S = 0.0f;
-    int A = INT_MAX;
-    for (int k = 0; k < kThreads / 64; ++k) {
-      S += ss[k];
-      A = min(A, sa[k]);
-    }
-    DecPartial pr;
-    pr.m = M;
-    pr.s = S;
-    pr.a = A;
-    pr.pad = 0;
-    a.part[(int64_t)row * a.nchunk + c] = pr;
   }
 }
 
-__global__ __launch_bounds__(256) void k_decode_select(DecArgs a) {
-  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + wv;
-  if (i >= a.n) return;
+// Running reduction of one thread over its elements, in increasing index
+// order: exact max `mt` with the start `vbest` of the first 16-byte vector
+// holding it, and the sum `s` of exp(x - mb / log2 e). The shift mb (log2
+// domain) is raised lazily, only when a vector's max exceeds it by more than
+// 8, so every term stays below 2^8 and the sum far from overflow. mb starts at
+// -FLT_MAX rather than -inf so that -inf elements contribute exp2(-inf) = 0.
+struct RowAcc {
+  float mt = -__builtin_inff();
+  int vbest = 0;
+  float mb = -FLT_MAX;
+  float s = 0.0f;
+};
+
+template <typename T>
+__device__ inline void fold_vector(const v4u& v, int e0, RowAcc& r) {
+  constexpr int N = Lanes<T>::N;
+  float f[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) f[k] = Lanes<T>::get(v, k);
+  float vm = f[0];
+#pragma unroll
+  for (int k = 1; k < N; ++k) vm = fmaxf(vm, f[k]);
+  if (vm > r.mt) {
+    r.mt = vm;
+    r.vbest = e0;
+  }
+  const float nb = vm * kLog2e;
+  if (nb > r.mb + 8.0f) {
+    r.s *= __builtin_amdgcn_exp2f(r.mb - nb);
+    r.mb = nb;
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int k = 0; k < N; ++k) acc += __builtin_amdgcn_exp2f(fmaf(f[k], kLog2e, -r.mb));
+  r.s += acc;
+}
+
+template <typename T>
+__device__ inline void fold_chunk(v4u (&buf)[kLoads], int v0, int V, int tid, RowAcc& r) {
+  constexpr int N = Lanes<T>::N;
+  mask_tail<T>(buf, v0, V, tid);
+#pragma unroll
+  for (int u = 0; u < kLoads; ++u) fold_vector<T>(buf[u], v0 + (u * kThreads + tid) * N, r);
+}
+
+// Selection of request i by one wave (lane j = block position j): merge the
+// row's part results, apply n = min(|M|, max(q_min, #{c >= tau})) to the
+// most confident positions (ties: smallest j), update tokens/mask in place.
+__device__ inline void select_request(const DecArgs& a, int i, int lane) {
   const Geo q = geo_of(a.reqs[i], a.L);
   const int j = lane;
   const int64_t cell = (int64_t)i * a.L + j;
@@ -167,17 +150,18 @@ __global__ __launch_bounds__(256) void k_decode_select(DecArgs a) {
   float conf = -1.0f;
   int arg = 0;
   if (m) {
-    const DecPartial* pp = a.part + cell * a.nchunk;
-    float M = pp[0].m;
-    arg = pp[0].a;
-    for (int c = 1; c < a.nchunk; ++c)
-      if (pp[c].m > M) {
-        M = pp[c].m;
-        arg = pp[c].a;
-      }
+    const DecPartial* pp = a.part + cell * a.parts;
+    float M = -__builtin_inff();
+    for (int p = 0; p < a.parts; ++p) M = fmaxf(M, pp[p].m);
     float S = 0.0f;
-    for (int c = 0; c < a.nchunk; ++c) S += pp[c].s * __builtin_amdgcn_exp2f((pp[c].m - M) * kLog2e);
+    int A = INT_MAX;
+    for (int p = 0; p < a.parts; ++p) {
+      const DecPartial pr = pp[p];
+      S += pr.s * __builtin_amdgcn_exp2f((pr.m - M) * kLog2e);
+      if (pr.m == M) A = min(A, pr.a);
+    }
     conf = 1.0f / S;
+    arg = A;
   }
   const unsigned long long bm = __ballot(m);
   const unsigned long long bt = __ballot(m && conf >= a.tau);
@@ -213,18 +197,101 @@ __global__ __launch_bounds__(256) void k_decode_select(DecArgs a) {
   }
 }
 
+// Stream NC chunks starting at chunk c0 (two register buffers; every load is
+// issued unconditionally, so only the buffer about to be folded is waited for).
+template <typename T, int NC>
+__device__ inline void stream_part(const T* x, int c0, int V, int tid, RowAcc& r) {
+  constexpr int CH = kDecChunkBytes / sizeof(T);
+  v4u buf[2][kLoads];
+  load_chunk<T>(buf[0], x, c0 * CH, V, tid);
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    if (k + 1 < NC) load_chunk<T>(buf[(k + 1) & 1], x, (c0 + k + 1) * CH, V, tid);
+    fold_chunk<T>(buf[k & 1], (c0 + k) * CH, V, tid, r);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_decode_parts(DecArgs a) {
+  constexpr int N = Lanes<T>::N;
+  constexpr int CH = kDecChunkBytes / sizeof(T);
+  static_assert(kDecPartChunks >= 1 && kDecPartChunks <= 4, "stream_part is instantiated for 1..4 chunks");
+  const int row = blockIdx.x / a.parts, part = blockIdx.x - row * a.parts;
+  const int i = row / a.L, j = row - i * a.L;
+  const Geo q = geo_of(a.reqs[i], a.L);
+  if (j >= q.B || a.masked[row] == 0) return;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const T* x = static_cast<const T*>(a.logits) + (int64_t)row * a.row_stride;
+  const int nchunk = (a.V + CH - 1) / CH;
+  const int c0 = part * kDecPartChunks;
+  const int nc = min(kDecPartChunks, nchunk - c0);   // >= 1: parts = ceil(nchunk / kDecPartChunks)
+
+  RowAcc r;
+  switch (nc) {
+    case 1: stream_part<T, 1>(x, c0, a.V, tid, r); break;
+    case 2: stream_part<T, (kDecPartChunks >= 2 ? 2 : 1)>(x, c0, a.V, tid, r); break;
+    case 3: stream_part<T, (kDecPartChunks >= 3 ? 3 : 1)>(x, c0, a.V, tid, r); break;
+    default: stream_part<T, kDecPartChunks>(x, c0, a.V, tid, r); break;
+  }
+  // part max and sum across the workgroup
+  __shared__ float sm[kThreads / 64];
+  __shared__ float ss[kThreads / 64];
+  __shared__ int sa[kThreads / 64];
+  const float wm = wave_max(r.mt);
+  if (lane == 0) sm[w] = wm;
+  __syncthreads();
+  float M = sm[0];
+#pragma unroll
+  for (int k = 1; k < kThreads / 64; ++k) M = fmaxf(M, sm[k]);
+  // r.mb <= r.mt * log2 e <= M * log2 e, so the factor is at most 1
+  const float sc = r.s * __builtin_amdgcn_exp2f(r.mb - M * kLog2e);
+  // smallest index holding M: threads whose max is M re-read the one vector
+  // where they first saw it
+  int arg = INT_MAX;
+  if (r.mt == M) {
+    const v4u v = ld16(x + r.vbest);
+#pragma unroll
+    for (int e = N - 1; e >= 0; --e)
+      if (Lanes<T>::get(v, e) == M && r.vbest + e < a.V) arg = r.vbest + e;
+  }
+  const float wsum = wave_sum(sc);
+  const int wa = wave_min_i(arg);
+  if (lane == 0) {
+    ss[w] = wsum;
+    sa[w] = wa;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float S = 0.0f;
+    int A = INT_MAX;
+    for (int k = 0; k < kThreads / 64; ++k) {
+      S += ss[k];
+      A = min(A, sa[k]);
+    }
+    DecPartial pr;
+    pr.m = M;
+    pr.s = S;
+    pr.a = A;
+    pr.pad = 0;
+    a.part[(int64_t)row * a.parts + part] = pr;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_decode_select(DecArgs a) {
+  select_request(a, blockIdx.x, threadIdx.x);
+}
+
 }  // namespace
 
 hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s) {
-  const int64_t rows = (int64_t)a.n * a.L;
-  const dim3 g1((unsigned)(rows * a.nchunk)), b1(kThreads);
+  const dim3 grid((unsigned)((int64_t)a.n * a.L * a.parts)), block(kThreads);
   if (dt == BS_BF16)
-    hipLaunchKernelGGL(k_decode_rows<uint16_t>, g1, b1, 0, s, a);
+    hipLaunchKernelGGL(k_decode_parts<uint16_t>, grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL(k_decode_rows<float>, g1, b1, 0, s, a);
+    hipLaunchKernelGGL(k_decode_parts<float>, grid, block, 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_decode_select, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_decode_select, dim3(a.n), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

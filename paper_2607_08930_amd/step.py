@@ -15,8 +15,8 @@ import numpy as np
 import torch
 
 from . import (BS_BF16, BS_F32, Context, bs_decode_workspace_bytes, bs_dual_cache_block_attention,
-               bs_gather_active_blocks, bs_kv_scatter_compact, bs_parallel_decode,
-               bs_scatter_active_blocks)
+               bs_gather_active_blocks_n, bs_kv_scatter_compact, bs_parallel_decode,
+               bs_scatter_active_blocks_n)
 
 
 def dt_code(dtype: str) -> int:
@@ -103,9 +103,9 @@ def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want
     n = len(reqs)
     L, R, W = st.L, st.R, st.W
     dt = dt_code(st.dtype)
-    bs_gather_active_blocks(ctx, reqs, L, R, W, st.tokens, st.tokens.stride(0) * 4, 4, st.tok_c, st.pos,
-                            stream=stream)
-    bs_gather_active_blocks(ctx, reqs, L, R, W, st.mask, st.mask.stride(0), 1, st.msk_c, None, stream=stream)
+    strides = [st.tokens.stride(0) * 4, st.mask.stride(0)]
+    bs_gather_active_blocks_n(ctx, reqs, L, R, W, [st.tokens, st.mask], strides, [4, 1], [st.tok_c, st.msk_c],
+                              st.pos, stream=stream)
     for lay in (st.layers if layers is None else layers):
         bs_dual_cache_block_attention(ctx, reqs, L, st.Hq, st.Hkv, st.D, dt, st.scale, lay.q, lay.k_new,
                                       lay.v_new, lay.k_cache, lay.v_cache, R, W, st.write_back, lay.out,
@@ -113,9 +113,8 @@ def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want
     bs_parallel_decode(ctx, reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c, st.tau,
                        st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen,
                        st.conf if want_conf else None, st.dec_ws, st.dec_ws.numel(), stream=stream)
-    bs_scatter_active_blocks(ctx, reqs, L, R, W, st.tok_c, 4, st.tokens, st.tokens.stride(0) * 4,
-                             stream=stream)
-    bs_scatter_active_blocks(ctx, reqs, L, R, W, st.msk_c, 1, st.mask, st.mask.stride(0), stream=stream)
+    bs_scatter_active_blocks_n(ctx, reqs, L, R, W, [st.tok_c, st.msk_c], [4, 1], [st.tokens, st.mask], strides,
+                               stream=stream)
 
 
 def compact(ctx: Context, segs: np.ndarray, n_layers: int, Hkv: int, D: int, dtype: str,

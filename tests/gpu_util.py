@@ -77,7 +77,8 @@ def check_attention(w, got, ref, reqs=None, label=""):
     return err, mx
 
 
-def run_decode(ctx, w, logits, tok_c, msk_c, *, tau=None, q_min=None, eos_id=None, reqs=None, dev_logits=None):
+def run_decode(ctx, w, logits, tok_c, msk_c, *, tau=None, q_min=None, eos_id=None, reqs=None, dev_logits=None,
+               ws=None):
     torch, bs, bstep = lazy()
     reqs = w.reqs if reqs is None else reqs
     n = len(reqs)
@@ -104,12 +105,12 @@ def run_decode(ctx, w, logits, tok_c, msk_c, *, tau=None, q_min=None, eos_id=Non
     eos = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
     conf = torch.full((n, w.L), float("nan"), dtype=torch.float32, device="cuda")
     wsb = bs.bs_decode_workspace_bytes(n, w.L, w.V, bstep.dt_code(w.dtype))
-    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    ws = torch.full((max(wsb, 16),), 0xAB, dtype=torch.uint8, device="cuda") if ws is None else ws
     bs.bs_parallel_decode(ctx, reqs, w.L, w.V, bstep.dt_code(w.dtype), dl, dl.stride(1), dt, dm, tau, q_min,
                           eos_id, nun, done, eos, conf, ws, wsb)
     torch.cuda.synchronize()
     return dict(tokens=dt.cpu().numpy(), masked=dm.cpu().numpy(), n_unmasked=nun.cpu().numpy(),
-                done=done.cpu().numpy(), eos_seen=eos.cpu().numpy(), conf=conf.cpu().numpy())
+                done=done.cpu().numpy(), eos_seen=eos.cpu().numpy(), conf=conf.cpu().numpy(), ws=ws)
 
 
 def exempt_requests(ref, reqs, L, tau):

@@ -65,6 +65,41 @@ def test_gather_scatter_workloads(ctx, cfg):
     assert np.array_equal(oracle.gather_active_blocks(w.reqs, w.L, msk)[0].astype(bool), blk)
 
 
+def test_gather_scatter_multi_tensor(ctx):
+    """Four tensors of element sizes 16, 4, 2, 1 with padded row strides move
+    in one launch exactly as four single-tensor calls would."""
+    torch, bs, _ = lazy()
+    say("[gather multi]")
+    w = synth.custom(8, 2, 2, 16, 50, "f32", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8], [1, 0, 1, 2, 0],
+                     W=40, rows=[2, 0, 4, 1, 3])
+    rng = np.random.default_rng(77)
+    ebs = [16, 4, 2, 1]
+    pads = [0, 3, 8, 5]                                   # extra row elements
+    boxes = [rng.integers(0, 256, size=(w.R, w.W + pd, eb), dtype=np.uint8) for eb, pd in zip(ebs, pads)]
+    dboxes = [torch.from_numpy(b).cuda() for b in boxes]
+    outs = [torch.full((w.n, w.L, eb), 0xCD, dtype=torch.uint8, device="cuda") for eb in ebs]
+    pos = torch.full((w.n, w.L), -9, dtype=torch.int32, device="cuda")
+    strides = [(w.W + pd) * eb for eb, pd in zip(ebs, pads)]
+    bs.bs_gather_active_blocks_n(ctx, w.reqs, w.L, w.R, w.W, dboxes, strides, ebs, outs, pos)
+    torch.cuda.synchronize()
+    for b, o in zip(boxes, outs):
+        ref, pos_ref = oracle.gather_active_blocks(w.reqs, w.L, b[:, :w.W])
+        np.testing.assert_array_equal(o.cpu().numpy(), ref)
+    np.testing.assert_array_equal(pos.cpu().numpy(), pos_ref)
+    ys = [rng.integers(0, 256, size=(w.n, w.L, eb), dtype=np.uint8) for eb in ebs]
+    bs.bs_scatter_active_blocks_n(ctx, w.reqs, w.L, w.R, w.W, [torch.from_numpy(y).cuda() for y in ys], ebs,
+                                  dboxes, strides)
+    torch.cuda.synchronize()
+    for b, y, d in zip(boxes, ys, dboxes):
+        exp = b.copy()
+        exp[:, :w.W] = oracle.scatter_active_blocks(w.reqs, w.L, y, b[:, :w.W])
+        np.testing.assert_array_equal(d.cpu().numpy(), exp)     # padding columns untouched
+    with pytest.raises(bs.BlockServeError, match="UNSUPPORTED"):
+        bs.bs_gather_active_blocks_n(ctx, w.reqs, w.L, w.R, w.W, dboxes[:2], strides[:2], [16, 3], outs[:2])
+    with pytest.raises(bs.BlockServeError, match="INVALID_ARG"):
+        bs.bs_gather_active_blocks_n(ctx, w.reqs, w.L, w.R, w.W, dboxes * 2, strides * 2, ebs * 2, outs * 2)
+
+
 def test_gather_empty_batch_is_noop(ctx):
     torch, bs, _ = lazy()
     d = torch.zeros((2, 8), dtype=torch.int32, device="cuda")
@@ -121,6 +156,27 @@ def test_decode_tiny_vocab_tail(ctx):
     _decode_case(ctx, w, "V=37 fp32")
     w = synth.custom(8, 2, 2, 16, 70000, "bf16", [3, 7], [16, 12], [1, 1])
     _decode_case(ctx, w, "V=70000 bf16 (3 chunks, ragged)")
+
+
+def test_decode_workspace_contents_ignored(ctx):
+    # the workspace carries part results between the call's two launches only:
+    # garbage on entry (NaN bit patterns, stale results of another step) must
+    # not change the outcome, over successive steps whose masked sets differ
+    torch, bs, bstep = lazy()
+    w = synth.workload(2, V=70000)          # bf16 rows of 5 chunks: 3 parts, the last one short
+    tok, msk, blk = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    logits = synth.gen_logits(w, np.ones_like(blk))
+    wsb = bs.bs_decode_workspace_bytes(w.n, w.L, w.V, bstep.dt_code(w.dtype))
+    ws = torch.full((wsb,), 0xFF, dtype=torch.uint8, device="cuda")
+    for step in range(3):
+        say(f"[decode ws step {step}] masked={int(msk_c.sum())}")
+        got = run_decode(ctx, w, logits, tok_c, msk_c, ws=ws)
+        ref = oracle.parallel_decode(w.reqs, w.L, logits, tok_c, msk_c, tau=w.tau, q_min=1, eos_id=-1,
+                                     dtype=w.dtype)
+        check_decode(w, got, ref, label=f"ws step {step}")
+        tok_c, msk_c = got["tokens"], got["masked"]
 
 
 def test_decode_rejects_unaligned_row_stride(ctx):

@@ -1,18 +1,19 @@
 """Benchmark of the mixed-state denoising step on one MI355X.
 
-One step = gather (token ids, mask bits) -> dual-cache block attention (every
-layer) -> parallel decode -> scatter (token ids, mask bits), all through
-libblockserve's C ABI on one stream; the block-boundary churn workload (5)
-adds the KV compaction first. Inputs are synthetic and resident in HBM before
-timing. Between steps (outside the per-step events) the decoded token/mask
-state is restored from pristine copies and a 512 MiB buffer is read, so the
-256 MB Infinity Cache holds none of the step's data (cold numbers). The sweep
-reads rather than writes: a written sweep would leave the cache full of dirty
-lines whose write-back would then be charged to the timed step.
+One step = dual-cache block attention (every layer) -> parallel decode with the
+token/mask gather and scatter fused in, enqueued by one bs_mixed_state_step
+call on one stream. Inputs are synthetic and resident in HBM before timing.
+Between steps (outside the per-step events) the decoded token/mask state is
+restored from pristine copies and a 512 MiB buffer is read, so the 256 MB
+Infinity Cache holds none of the step's data (cold numbers). The sweep reads
+rather than writes: a written sweep would leave the cache full of dirty lines
+whose write-back would then be charged to the timed step.
 
-Prints ONE JSON line (rank 0): positions/s, ms per step, per-kernel event
-times, algorithmic HBM traffic, the roofline of the dominant kernel and the
-CPU oracle timed on a bounded sample of the same workload.
+Per-phase times (attention over all layers, decode row reductions, selection)
+come from the library's event ring, recorded on the step's stream during the
+timed steps. Prints ONE JSON line: positions/s, ms per step, phase times,
+algorithmic HBM traffic, the roofline of the dominant kernel and the CPU oracle
+timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -72,8 +73,9 @@ def masked_rows(blk):
     return int(blk.sum())
 
 
-def cpu_baseline(w, host, budget_s=12.0):
-    """The oracle as it stands, timed on this host on the same inputs."""
+def cpu_baseline(w, host, budget_s=12.0, max_reps=200):
+    """The oracle as it stands, timed on this host on the same inputs: whole
+    oracle steps are repeated until about budget_s seconds have passed."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -88,11 +90,11 @@ def cpu_baseline(w, host, budget_s=12.0):
                                 tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 3:
+        if el >= budget_s or reps >= max_reps:
             break
-    return {"value": positions * reps / el, "unit": "positions/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{reps} full oracle step(s) of the same workload ({positions} positions, "
-                      f"{w.layers} layer(s)), fp64 NumPy, {el:.1f} s"}
+    return {"value": round(positions * reps / el, 1), "unit": "positions/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps} whole oracle steps of the same workload ({positions} positions, "
+                      f"{w.layers} layer(s) each), fp64 NumPy, {el:.1f} s"}
 
 
 def main():
@@ -100,12 +102,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload 1-4 (2 = LLaDA-8B-shaped layer)")
+    ap.add_argument("--config", type=int, default=2, help="workload 1-4 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+        print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
               file=sys.stderr, flush=True)
         sys.exit(2)
 
@@ -122,33 +124,15 @@ def main():
     ab = algorithmic_bytes(w)
     nmask = masked_rows(host["blk"])
     logits_bytes = nmask * w.V * w.elem
-    small_bytes = ab["positions"] * (5 + 5 + 4 + 5 + 5)
+    small_bytes = ab["positions"] * (4 + 4 + 1 + 1 + 4)        # token r/w, mask r/w, position id
     step_bytes = ab["attn"] + logits_bytes + small_bytes
     tok0, msk0 = st.tokens.clone(), st.mask.clone()
     flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")    # 512 MiB, swept by reading
     stream = torch.cuda.current_stream()
     ctx = bs.Context(0)
 
-    names = ["gather", "attention", "decode", "scatter"]
-
-    def one_step(evs=None):
-        L, R, W = st.L, st.R, st.W
-        dt = bstep.dt_code(st.dtype)
-        if evs: evs[0].record(stream)
-        bs.bs_gather_active_blocks_n(ctx, w.reqs, L, R, W, [st.tokens, st.mask], [W * 4, W], [4, 1],
-                                     [st.tok_c, st.msk_c], st.pos)
-        if evs: evs[1].record(stream)
-        for lay in st.layers:
-            bs.bs_dual_cache_block_attention(ctx, w.reqs, L, st.Hq, st.Hkv, st.D, dt, 0.0, lay.q, lay.k_new,
-                                             lay.v_new, lay.k_cache, lay.v_cache, R, W, 1, lay.out)
-        if evs: evs[2].record(stream)
-        bs.bs_parallel_decode(ctx, w.reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c,
-                              st.tau, st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, None,
-                              st.dec_ws, st.dec_ws.numel())
-        if evs: evs[3].record(stream)
-        bs.bs_scatter_active_blocks_n(ctx, w.reqs, L, R, W, [st.tok_c, st.msk_c], [4, 1], [st.tokens, st.mask],
-                                      [W * 4, W])
-        if evs: evs[4].record(stream)
+    def one_step():
+        bstep.run_step(ctx, st, w.reqs, stream=stream)
 
     def reset():
         st.tokens.copy_(tok0)
@@ -161,32 +145,35 @@ def main():
         one_step()
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps); timing {args.steps}", file=sys.stderr, flush=True)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    bs.bs_profile_begin(ctx, args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         reset()
-        one_step(evs[k])
+        evs[k][0].record(stream)
+        one_step()
+        evs[k][1].record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / args.steps * 1e3
-    per = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(4)] for k in range(args.steps)])
-    step_ms = per.sum(axis=1)
+    phases = bs.bs_profile_end(ctx, args.steps)              # [steps][attention, decode_rows, decode_select]
+    step_ms = np.array([a.elapsed_time(b) for a, b in evs])
     ms = float(np.median(step_ms))
-    attn_ms = float(np.median(per[:, 1])) / w.layers
-    dec_ms = float(np.median(per[:, 2]))
+    attn_ms = float(np.median(phases[:, 0])) / w.layers       # one attention launch
+    rows_ms = float(np.median(phases[:, 1]))
     value = ab["positions"] / (ms / 1e3)
     attn_gbs = ab["attn_per_layer"] / (attn_ms / 1e3) / 1e9
-    dec_gbs = logits_bytes / (dec_ms / 1e3) / 1e9
+    dec_gbs = logits_bytes / (rows_ms / 1e3) / 1e9
     attn_dominant = ab["attn"] >= logits_bytes
     if attn_dominant:
-        roof = {"kernel": "k_attn_bf16" if w.dtype == "bf16" else "k_attn_f32", "bound": "hbm",
+        roof = {"kernel": "k_attn_bf16_wave" if w.dtype == "bf16" else "k_attn_f32", "bound": "hbm",
                 "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None,
                 "algorithmic_bytes_per_launch": ab["attn_per_layer"], "avg_launch_ms": round(attn_ms, 5)}
     else:
-        roof = {"kernel": "k_decode_rows", "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
+        roof = {"kernel": "k_decode_parts", "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                "algorithmic_bytes_per_launch": logits_bytes, "avg_launch_ms": round(dec_ms, 5)}
+                "algorithmic_bytes_per_launch": logits_bytes, "avg_launch_ms": round(rows_ms, 5)}
     ctx.close()
     res = {
         "metric": "denoised block positions/s per mixed-state step",
@@ -199,8 +186,8 @@ def main():
                    "cache": "warm" if args.warm else "cold (512 MiB read sweep between steps)"},
         "hbm": {"algorithmic_bytes_per_step": step_bytes, "achieved_GBps": round(step_bytes / (ms / 1e3) / 1e9, 1),
                 "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
-        "kernels_ms": {n_: round(float(np.median(per[:, i])), 5) for i, n_ in enumerate(names)},
-        "kernel_GBps": {"attention": round(attn_gbs, 1), "decode": round(dec_gbs, 1)},
+        "phases_ms": {n_: round(float(np.median(phases[:, i])), 5) for i, n_ in enumerate(bs.PROFILE_PHASES)},
+        "kernel_GBps": {"attention": round(attn_gbs, 1), "decode_rows": round(dec_gbs, 1)},
         "attention_tflops": round(ab["attn_flops"] / w.layers / (attn_ms / 1e3) / 1e12, 2),
         "wall_ms_per_step_incl_restore": round(wall, 5),
         "step_ms_p10_p90": [round(float(np.percentile(step_ms, 10)), 5), round(float(np.percentile(step_ms, 90)), 5)],

@@ -226,6 +226,47 @@ int bs_kv_scatter_compact(bs_ctx* ctx, const bs_copy_seg* segs, int nseg, int n_
                           void* dst_k, void* dst_v, int64_t dst_layer_stride, int R_dst, int W_dst,
                           void* stream);
 
+/*
+ * One mixed-state denoising step in one call (Algorithm 1's inner loop body;
+ * paragraph "Vectorized mixed-schedule execution": every request advances its
+ * own active block in the same batched step). Enqueues, in order: K2 for each
+ * layer l < n_layers on that layer's tensors (q[l], k_new[l], v_new[l],
+ * k_cache[l], v_cache[l], out[l]: host arrays of n_layers device pointers, each
+ * with the layout and rules of bs_dual_cache_block_attention), then K3 on the
+ * logits. K3 reads and updates the block cells of the DENSE token and mask
+ * boxes directly: tokens / masked are [R][W] with row strides
+ * tokens_row_stride / masked_row_stride ELEMENTS (>= W), block cell j of
+ * request i at (row_i, off_i + s_i + j). The result equals K1 gather of tokens
+ * and mask, K2 per layer, K3 on the compact state, then K1^-1 scatter; only
+ * the gather/scatter launches are saved. pos_out ([n][L] int32, may be NULL)
+ * receives s_i + j for j < B_i and -1 beyond. conf_out as for K3 ([n][L]).
+ * Other arguments as for K2 and K3 (n_layers == 0 runs K3 alone); ws is K3's
+ * workspace: bs_decode_workspace_bytes(n, L, V, logits_dt) bytes. All checks
+ * run before anything is enqueued.
+ */
+int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
+                        int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
+                        const void* const* k_new, const void* const* v_new, void* const* k_cache,
+                        void* const* v_cache, void* const* out, int V, bs_dtype logits_dt, const void* logits,
+                        int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
+                        int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
+                        uint8_t* done, uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/*
+ * Phase timing of bs_mixed_state_step (a trace facility; no method content).
+ * bs_profile_begin arms a ring of max_steps steps: each following step call
+ * records BS_PROFILE_PHASES + 1 HIP events on its stream (before attention,
+ * after attention, after the decode row reductions, after the selection),
+ * until max_steps steps are recorded. bs_profile_end waits for the recorded
+ * events and writes phase_ms[k][ph] (k < *n_steps, ph < BS_PROFILE_PHASES:
+ * attention over all layers, decode row reductions, selection) for up to
+ * max_steps steps, then disarms. Events are created once and reused.
+ */
+#define BS_PROFILE_PHASES 3
+int bs_profile_begin(bs_ctx* ctx, int max_steps);
+int bs_profile_end(bs_ctx* ctx, float* phase_ms, int max_steps, int* n_steps);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,7 +21,8 @@ __all__ = [
     "REQ_DTYPE", "SEG_DTYPE", "BS_F32", "BS_BF16", "BlockServeError", "Context", "lib", "LIB_PATH",
     "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
     "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_gather_active_blocks_n",
-    "bs_scatter_active_blocks_n", "bs_attention_workspace_bytes",
+    "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_profile_begin", "bs_profile_end",
+    "bs_attention_workspace_bytes",
     "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
     "bs_kv_scatter_compact",
 ]
@@ -74,6 +75,11 @@ _SIGS = {
     "bs_scatter_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i64, _vp]),
     "bs_gather_active_blocks_n": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "bs_scatter_active_blocks_n": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "bs_mixed_state_step": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32,
+                                   _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i64, _vp, _i64, _vp, _i64,
+                                   _f32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bs_profile_begin": (_i32, [_vp, _i32]),
+    "bs_profile_end": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_i32)]),
     "bs_attention_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "bs_dual_cache_block_attention": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                              _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
@@ -261,3 +267,34 @@ def bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt, src_k, src_v, src_lay
         _ptr(ctx), _ptr(s), len(s), n_layers, Hkv, D, dt, _ptr(src_k), _ptr(src_v), int(src_layer_stride),
         R_src, W_src, _ptr(stg_k), _ptr(stg_v), int(stg_layer_stride), R_stg, W_stg, _ptr(dst_k),
         _ptr(dst_v), int(dst_layer_stride), R_dst, W_dst, _stream(stream)), ctx)
+
+
+def bs_mixed_state_step(ctx, reqs, L, R, W, layers, Hq, Hkv, D, dt, scale, write_back, V, logits_dt, logits,
+                        logits_row_stride, tokens, tokens_row_stride, masked, masked_row_stride, tau, q_min, eos_id,
+                        n_unmasked, done, eos_seen, conf_out, pos_out, ws, ws_bytes, stream=None):
+    """``layers``: sequence of (q, k_new, v_new, k_cache, v_cache, out) per layer.
+
+    Row strides of tokens/masked are in elements."""
+    r = _host(reqs, REQ_DTYPE)
+    nl = len(layers)
+    arrs = [(_vp * max(nl, 1))(*[_ptr(lay[t]) for lay in layers]) for t in range(6)]
+    return _check(lib.bs_mixed_state_step(_ptr(ctx), _ptr(r), len(r), L, R, W, nl, Hq, Hkv, D, dt, scale,
+                                          int(write_back), *arrs, V, logits_dt, _ptr(logits), logits_row_stride,
+                                          _ptr(tokens), tokens_row_stride, _ptr(masked), masked_row_stride, tau,
+                                          q_min, eos_id, _ptr(n_unmasked), _ptr(done), _ptr(eos_seen),
+                                          _ptr(conf_out), _ptr(pos_out), _ptr(ws), ws_bytes, _stream(stream)), ctx)
+
+
+PROFILE_PHASES = ("attention", "decode_rows", "decode_select")
+
+
+def bs_profile_begin(ctx, max_steps: int) -> None:
+    _check(lib.bs_profile_begin(_ptr(ctx), max_steps), ctx)
+
+
+def bs_profile_end(ctx, max_steps: int) -> np.ndarray:
+    """Per-step phase durations in ms, shape [steps][len(PROFILE_PHASES)]."""
+    out = np.zeros((max(max_steps, 1), len(PROFILE_PHASES)), np.float32)
+    n = _i32(0)
+    _check(lib.bs_profile_end(_ptr(ctx), out.ctypes.data, max_steps, ctypes.byref(n)), ctx)
+    return out[:n.value].copy()

@@ -100,9 +100,31 @@ struct DecArgs {
   float* conf_out;
   int parts;       // parts per row
   DecPartial* part;
+  // tokens/masked layout: compact [n][L] (dense == 0), or the dense [R][W]
+  // boxes with these row strides in elements, block cell j of request i at
+  // (row_i, off_i + s_i + j)
+  int dense;
+  int64_t tok_rs, msk_rs;
+  int32_t* pos_out;  // [n][L] or NULL: s_i + j for j < B_i, else -1
 };
 
 hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s);
+
+// launch_decode with mark(2) after the row reductions and mark(3) after the
+// selection (the step's phase-timing event indices); mark returns a hipError_t.
+template <class Mark>
+hipError_t launch_decode_marked(const DecArgs& a, bs_dtype dt, hipStream_t s, Mark mark);
+hipError_t launch_decode_rows(const DecArgs& a, bs_dtype dt, hipStream_t s);
+hipError_t launch_decode_select(const DecArgs& a, hipStream_t s);
+
+template <class Mark>
+hipError_t launch_decode_marked(const DecArgs& a, bs_dtype dt, hipStream_t s, Mark mark) {
+  hipError_t e = launch_decode_rows(a, dt, s);
+  if (e == hipSuccess) e = mark(2);
+  if (e == hipSuccess) e = launch_decode_select(a, s);
+  if (e == hipSuccess) e = mark(3);
+  return e;
+}
 
 // ---------------------------------------------------------------- gather / scatter
 constexpr int kMaxGather = 4;  // tensors moved by one gather/scatter launch

@@ -47,11 +47,22 @@ uint64_t fnv1a(const void* p, size_t n) {
 
 }  // namespace
 
+// Phase timing of bs_mixed_state_step: kProfPhases + 1 events per step
+// (before attention, after attention, after the row reductions, after selection).
+constexpr int kProfPhases = BS_PROFILE_PHASES;
+struct Prof {
+  std::vector<hipEvent_t> ev;
+  int cap = 0;     // steps the ring holds
+  int used = 0;    // steps recorded since bs_profile_begin
+  bool on = false;
+};
+
 struct bs_ctx {
   int device = 0;
   Slot slots[kSlots];
   int next = 0;
   std::string err;
+  Prof prof;
 };
 
 namespace {
@@ -208,6 +219,123 @@ int finish(bs_ctx* c, Slot* sl, hipStream_t s, hipError_t launch, const char* wh
 
 int dtype_bytes(bs_dtype dt) { return dt == BS_F32 ? 4 : (dt == BS_BF16 ? 2 : 0); }
 
+// ---- attention helpers shared by the K2 entry point and the fused step
+int check_attention(bs_ctx* c, int n, int L, int Hq, int Hkv, int D, bs_dtype dt) {
+  (void)n;
+  if (dt != BS_F32 && dt != BS_BF16) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)dt);
+  if (Hq < 1 || Hkv < 1 || D < 1) return fail(c, BS_ERR_INVALID_ARG, "Hq, Hkv, D must be >= 1");
+  if (Hq % Hkv) return fail(c, BS_ERR_UNSUPPORTED, "Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
+  const int G = Hq / Hkv, RB = (L + 31) / 32;
+  if (dt == BS_F32 && (D % 4 || D > 256))
+    return fail(c, BS_ERR_UNSUPPORTED, "fp32 path needs D %% 4 == 0 and D <= 256 (D=%d)", D);
+  if (dt == BS_BF16) {
+    if (D != 64 && D != 128) return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs D in {64, 128} (D=%d)", D);
+    if (L > 64 || G * RB > 8)
+      return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs L <= 64 and (Hq/Hkv)*ceil(L/32) <= 8 (got %d)", G * RB);
+  }
+  return BS_OK;
+}
+
+// layer < 0: the single-layer entry point (no layer in the message)
+int check_attention_tensors(bs_ctx* c, const void* q, const void* k_new, const void* v_new, const void* k_cache,
+                            const void* v_cache, const void* out, int layer) {
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !out)
+    return layer < 0 ? fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL")
+                     : fail(c, BS_ERR_INVALID_ARG, "layer %d: tensor pointer is NULL", layer);
+  if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(out, 16))
+    return layer < 0 ? fail(c, BS_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned")
+                     : fail(c, BS_ERR_INVALID_ARG, "layer %d: tensor pointers must be 16-byte aligned", layer);
+  return BS_OK;
+}
+
+// Descriptors, then (bf16) the (request, KV head) work items, longest rows
+// first: neighbours in a workgroup have similar lengths and the tail of the
+// grid is made of short items.
+void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hkv, bs_dtype dt) {
+  blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
+  if (dt == BS_BF16) {
+    std::vector<AttnItem> items;
+    items.reserve((size_t)n * Hkv);
+    for (int i = 0; i < n; ++i) {
+      const Geo gq = geo_of(reqs[i], L);
+      for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, 0});
+    }
+    std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
+    blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * items.size());
+    blob.meta[2] = (int)items.size();
+  }
+}
+
+AttnArgs attention_args(const Slot* sl, int L, int Hq, int Hkv, int D, int R, int W, float scale, int write_back) {
+  const char* base = static_cast<const char*>(sl->d);
+  AttnArgs a{};
+  a.reqs = reinterpret_cast<const bs_req_desc*>(base + sl->meta[0]);
+  a.items = reinterpret_cast<const AttnItem*>(base + sl->meta[1]);
+  a.n_items = sl->meta[2];
+  a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = Hq / Hkv; a.RB = (L + 31) / 32; a.R = R; a.W = W;
+  a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
+  a.scale_log2e = a.scale * 1.4426950408889634f;
+  a.write_back = write_back ? 1 : 0;
+  return a;
+}
+
+// ---- decode helpers shared by the K3 entry point and the fused step
+size_t decode_ws_bytes(int n, int L, int V, bs_dtype dt) {
+  if (n <= 0 || L <= 0 || V <= 0 || dtype_bytes(dt) == 0) return 0;
+  return dec_workspace_bytes(n, L, dec_parts(V, dtype_bytes(dt)));
+}
+
+int check_decode(bs_ctx* c, int n, int L, int V, bs_dtype logits_dt, int64_t logits_row_stride, float tau,
+                 int q_min, const void* ws, size_t ws_bytes) {
+  const int eb = dtype_bytes(logits_dt);
+  if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)logits_dt);
+  if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
+  if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
+  if ((int64_t)n * L * dec_parts(V, eb) > INT32_MAX)
+    return fail(c, BS_ERR_UNSUPPORTED, "n * L * row parts exceeds the launch grid");
+  if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
+  if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
+  if (logits_row_stride < V || (logits_row_stride * eb) % 16)
+    return fail(c, BS_ERR_INVALID_ARG, "logits row stride %lld must be >= V and a multiple of 16 bytes",
+                (long long)logits_row_stride);
+  const size_t need = decode_ws_bytes(n, L, V, logits_dt);
+  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  return BS_OK;
+}
+
+int check_decode_tensors(bs_ctx* c, const void* logits, const int32_t* tokens, const uint8_t* masked,
+                         const int32_t* n_unmasked, const uint8_t* done, const uint8_t* eos_seen,
+                         const float* conf_out, const int32_t* pos_out, const void* ws) {
+  if (!logits || !tokens || !masked || !n_unmasked || !done || !eos_seen)
+    return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(logits, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) || !aligned(ws, 16) ||
+      (conf_out && !aligned(conf_out, 4)) || (pos_out && !aligned(pos_out, 4)))
+    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (logits and ws need 16 bytes)");
+  return BS_OK;
+}
+
+DecArgs decode_args(const bs_req_desc* dreqs, int n, int L, int V, bs_dtype logits_dt, const void* logits,
+                    int64_t logits_row_stride, float tau, int q_min, int eos_id, int32_t* n_unmasked,
+                    uint8_t* done, uint8_t* eos_seen, float* conf_out, void* ws) {
+  DecArgs a{};
+  a.reqs = dreqs;
+  a.n = n; a.L = L; a.V = V;
+  a.logits = logits; a.row_stride = logits_row_stride;
+  a.tau = tau; a.q_min = q_min; a.eos_id = eos_id;
+  a.n_unmasked = n_unmasked; a.done = done; a.eos_seen = eos_seen; a.conf_out = conf_out;
+  a.parts = dec_parts(V, dtype_bytes(logits_dt));
+  a.part = static_cast<DecPartial*>(ws);
+  return a;
+}
+
+// ---- phase timing of the fused step
+hipError_t prof_mark(bs_ctx* c, int phase, hipStream_t s) {
+  Prof& p = c->prof;
+  if (!p.on || p.used >= p.cap) return hipSuccess;
+  return hipEventRecord(p.ev[(size_t)p.used * (kProfPhases + 1) + phase], s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -228,6 +356,7 @@ int bs_create(bs_ctx** out, int device) {
 int bs_destroy(bs_ctx* c) {
   if (!c) return BS_OK;
   DeviceGuard dg(c->device);
+  for (hipEvent_t e : c->prof.ev) (void)hipEventDestroy(e);
   for (Slot& sl : c->slots) {
     if (sl.live) (void)hipEventSynchronize(sl.done);
     if (sl.d) (void)hipFree(sl.d);
@@ -343,65 +472,29 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
   int st = check_reqs(c, reqs, n, L, R, W);
   if (st) return st;
-  if (dt != BS_F32 && dt != BS_BF16) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)dt);
-  if (Hq < 1 || Hkv < 1 || D < 1) return fail(c, BS_ERR_INVALID_ARG, "Hq, Hkv, D must be >= 1");
-  if (Hq % Hkv) return fail(c, BS_ERR_UNSUPPORTED, "Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
-  const int G = Hq / Hkv, RB = (L + 31) / 32;
-  if (dt == BS_F32 && (D % 4 || D > 256)) return fail(c, BS_ERR_UNSUPPORTED, "fp32 path needs D %% 4 == 0 and D <= 256 (D=%d)", D);
-  if (dt == BS_BF16) {
-    if (D != 64 && D != 128) return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs D in {64, 128} (D=%d)", D);
-    if (L > 64 || G * RB > 8)
-      return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs L <= 64 and (Hq/Hkv)*ceil(L/32) <= 8 (got %d)", G * RB);
-  }
+  st = check_attention(c, n, L, Hq, Hkv, D, dt);
+  if (st) return st;
   const size_t need = bs_attention_workspace_bytes(reqs, n, L, Hq, Hkv, D, dt);
   if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   if (n == 0) return BS_OK;
-  if (!q || !k_new || !v_new || !k_cache || !v_cache || !out) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
-  if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) ||
-      !aligned(v_cache, 16) || !aligned(out, 16))
-    return fail(c, BS_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  st = check_attention_tensors(c, q, k_new, v_new, k_cache, v_cache, out, -1);
+  if (st) return st;
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-
   Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n), [&](Blob& blob) {
-    blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
-    if (dt == BS_BF16) {
-      std::vector<AttnItem> items;
-      items.reserve((size_t)n * Hkv);
-      for (int i = 0; i < n; ++i) {
-        const Geo gq = geo_of(reqs[i], L);
-        for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, 0});
-      }
-      // longest rows first: neighbours in a workgroup have similar lengths and
-      // the tail of the grid is made of short items
-      std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
-      blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * items.size());
-      blob.meta[2] = (int)items.size();
-    }
-  }, &sl);
+  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hkv, dt); }, &sl);
   if (st) return st;
-  const char* base = static_cast<const char*>(sl->d);
-  AttnArgs a{};
-  a.reqs = reinterpret_cast<const bs_req_desc*>(base + sl->meta[0]);
-  a.items = reinterpret_cast<const AttnItem*>(base + sl->meta[1]);
-  a.n_items = sl->meta[2];
-  a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = G; a.RB = RB; a.R = R; a.W = W;
-  a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
-  a.scale_log2e = a.scale * 1.4426950408889634f;
+  AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);
   a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
-  a.write_back = write_back ? 1 : 0;
   (void)ws;
   hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
   return finish(c, sl, s, e, "attention launch");
 }
 
 // ------------------------------------------------------------------ K3
-size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype dt) {
-  if (n <= 0 || L <= 0 || V <= 0 || dtype_bytes(dt) == 0) return 0;
-  return dec_workspace_bytes(n, L, dec_parts(V, dtype_bytes(dt)));
-}
+size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype dt) { return decode_ws_bytes(n, L, V, dt); }
 
 int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
                        bs_dtype logits_dt, const void* logits, int64_t logits_row_stride,
@@ -418,41 +511,121 @@ int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
     if (r.p < 0 || r.g < 1 || r.k < 0 || r.k >= K)
       return fail(c, BS_ERR_DESCRIPTOR, "request %d: p=%d g=%d k=%d invalid for L=%d", i, r.p, r.g, r.k, L);
   }
-  const int eb = dtype_bytes(logits_dt);
-  if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)logits_dt);
-  if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
-  if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
-  if ((int64_t)n * L * dec_parts(V, dtype_bytes(logits_dt)) > INT32_MAX)
-    return fail(c, BS_ERR_UNSUPPORTED, "n * L * row parts exceeds the launch grid");
-  if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
-  if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
-  if (logits_row_stride < V || (logits_row_stride * eb) % 16)
-    return fail(c, BS_ERR_INVALID_ARG, "logits row stride %lld must be >= V and a multiple of 16 bytes",
-                (long long)logits_row_stride);
-  const size_t need = bs_decode_workspace_bytes(n, L, V, logits_dt);
-  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  int st = check_decode(c, n, L, V, logits_dt, logits_row_stride, tau, q_min, ws, ws_bytes);
+  if (st) return st;
   if (n == 0) return BS_OK;
-  if (!logits || !tokens || !masked || !n_unmasked || !done || !eos_seen)
-    return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
-  if (!aligned(logits, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) || !aligned(ws, 16) ||
-      (conf_out && !aligned(conf_out, 4)))
-    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (logits and ws need 16 bytes)");
+  st = check_decode_tensors(c, logits, tokens, masked, n_unmasked, done, eos_seen, conf_out, nullptr, ws);
+  if (st) return st;
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  int st = upload_reqs(c, s, reqs, n, &sl);
+  st = upload_reqs(c, s, reqs, n, &sl);
   if (st) return st;
-  DecArgs a{};
-  a.reqs = static_cast<const bs_req_desc*>(sl->d);
-  a.n = n; a.L = L; a.V = V;
-  a.logits = logits; a.row_stride = logits_row_stride;
-  a.tokens = tokens; a.masked = masked; a.tau = tau; a.q_min = q_min; a.eos_id = eos_id;
-  a.n_unmasked = n_unmasked; a.done = done; a.eos_seen = eos_seen; a.conf_out = conf_out;
-  a.parts = dec_parts(V, dtype_bytes(logits_dt));
-  a.part = static_cast<DecPartial*>(ws);
+  DecArgs a = decode_args(static_cast<const bs_req_desc*>(sl->d), n, L, V, logits_dt, logits, logits_row_stride,
+                          tau, q_min, eos_id, n_unmasked, done, eos_seen, conf_out, ws);
+  a.tokens = tokens; a.masked = masked;
   hipError_t e = launch_decode(a, logits_dt, s);
   return finish(c, sl, s, e, "decode launch");
+}
+
+// ------------------------------------------------------------------ fused step
+int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
+                        int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
+                        const void* const* k_new, const void* const* v_new, void* const* k_cache,
+                        void* const* v_cache, void* const* out, int V, bs_dtype logits_dt, const void* logits,
+                        int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
+                        int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
+                        uint8_t* done, uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  int st = check_reqs(c, reqs, n, L, R, W);
+  if (st) return st;
+  if (n_layers < 0) return fail(c, BS_ERR_INVALID_ARG, "n_layers < 0");
+  if (n_layers > 0) {
+    st = check_attention(c, n, L, Hq, Hkv, D, dt);
+    if (st) return st;
+  }
+  st = check_decode(c, n, L, V, logits_dt, logits_row_stride, tau, q_min, ws, ws_bytes);
+  if (st) return st;
+  if (tokens_row_stride < W || masked_row_stride < W)
+    return fail(c, BS_ERR_INVALID_ARG, "token/mask row strides must be >= W");
+  if (n == 0) return BS_OK;
+  if (n_layers > 0 && (!q || !k_new || !v_new || !k_cache || !v_cache || !out))
+    return fail(c, BS_ERR_INVALID_ARG, "layer pointer array is NULL");
+  for (int l = 0; l < n_layers; ++l) {
+    st = check_attention_tensors(c, q[l], k_new[l], v_new[l], k_cache[l], v_cache[l], out[l], l);
+    if (st) return st;
+  }
+  st = check_decode_tensors(c, logits, tokens, masked, n_unmasked, done, eos_seen, conf_out, pos_out, ws);
+  if (st) return st;
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hkv, dt); }, &sl);
+  if (st) return st;
+  hipError_t e = prof_mark(c, 0, s);
+  AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);
+  for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+    a.q = q[l]; a.k_new = k_new[l]; a.v_new = v_new[l]; a.k_cache = k_cache[l]; a.v_cache = v_cache[l]; a.out = out[l];
+    e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
+  }
+  if (e == hipSuccess) e = prof_mark(c, 1, s);
+  if (e == hipSuccess) {
+    DecArgs d = decode_args(a.reqs, n, L, V, logits_dt, logits, logits_row_stride, tau, q_min, eos_id, n_unmasked,
+                            done, eos_seen, conf_out, ws);
+    d.tokens = tokens; d.masked = masked;
+    d.dense = 1; d.tok_rs = tokens_row_stride; d.msk_rs = masked_row_stride;
+    d.pos_out = pos_out;
+    e = launch_decode_marked(d, logits_dt, s, [&](int ph) { return prof_mark(c, ph, s); });
+  }
+  if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;
+  return finish(c, sl, s, e, "step launch");
+}
+
+int bs_profile_begin(bs_ctx* c, int max_steps) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  if (max_steps < 1 || max_steps > 1 << 16) return fail(c, BS_ERR_INVALID_ARG, "max_steps=%d outside [1, 65536]", max_steps);
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  Prof& p = c->prof;
+  const size_t need = (size_t)max_steps * (kProfPhases + 1);
+  while (p.ev.size() < need) {
+    hipEvent_t e = nullptr;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return hip_fail(c, r, "hipEventCreate(profile)");
+    p.ev.push_back(e);
+  }
+  p.cap = max_steps;
+  p.used = 0;
+  p.on = true;
+  return BS_OK;
+}
+
+int bs_profile_end(bs_ctx* c, float* phase_ms, int max_steps, int* n_steps) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  if (!n_steps || (max_steps > 0 && !phase_ms)) return fail(c, BS_ERR_INVALID_ARG, "output pointer is NULL");
+  Prof& p = c->prof;
+  if (!p.on) return fail(c, BS_ERR_INVALID_ARG, "profiling was not started");
+  p.on = false;
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  const int m = std::min(p.used, std::max(max_steps, 0));
+  for (int k = 0; k < m; ++k) {
+    hipEvent_t* ev = &p.ev[(size_t)k * (kProfPhases + 1)];
+    hipError_t r = hipEventSynchronize(ev[kProfPhases]);
+    if (r != hipSuccess) return hip_fail(c, r, "hipEventSynchronize(profile)");
+    for (int ph = 0; ph < kProfPhases; ++ph) {
+      float ms = 0.0f;
+      r = hipEventElapsedTime(&ms, ev[ph], ev[ph + 1]);
+      if (r != hipSuccess) return hip_fail(c, r, "hipEventElapsedTime(profile)");
+      phase_ms[(size_t)k * kProfPhases + ph] = ms;
+    }
+  }
+  *n_steps = m;
+  return BS_OK;
 }
 
 // ------------------------------------------------------------------ K4

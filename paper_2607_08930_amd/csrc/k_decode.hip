@@ -141,12 +141,20 @@ __device__ inline void fold_chunk(v4u (&buf)[kLoads], int v0, int V, int tid, Ro
 // Selection of request i by one wave (lane j = block position j): merge the
 // row's part results, apply n = min(|M|, max(q_min, #{c >= tau})) to the
 // most confident positions (ties: smallest j), update tokens/mask in place.
+// Cell of block position j < B_i of request i in the token / mask state.
+__device__ inline int64_t state_cell(const DecArgs& a, const bs_req_desc& r, const Geo& q, int i, int j, int64_t rs) {
+  return a.dense ? (int64_t)r.row * rs + r.off + q.s + j : (int64_t)i * a.L + j;
+}
+
 __device__ inline void select_request(const DecArgs& a, int i, int lane) {
-  const Geo q = geo_of(a.reqs[i], a.L);
+  const bs_req_desc rq = a.reqs[i];
+  const Geo q = geo_of(rq, a.L);
   const int j = lane;
-  const int64_t cell = (int64_t)i * a.L + j;
+  const int64_t cell = (int64_t)i * a.L + j;   // compact index: logits rows, part results, conf_out
   const bool inb = j < q.B;
-  const bool m = inb && a.masked[cell] != 0;
+  const int64_t tc = inb ? state_cell(a, rq, q, i, j, a.tok_rs) : 0;
+  const int64_t mc = inb ? state_cell(a, rq, q, i, j, a.msk_rs) : 0;
+  const bool m = inb && a.masked[mc] != 0;
   float conf = -1.0f;
   int arg = 0;
   if (m) {
@@ -177,16 +185,19 @@ __device__ inline void select_request(const DecArgs& a, int i, int lane) {
   const bool sel = m && rank < nsel;
   int tok = 0;
   bool still = false;
-  if (j < a.L) {
-    tok = a.tokens[cell];
-    still = a.masked[cell] != 0;
+  if (inb) {
+    tok = a.tokens[tc];
+    still = a.masked[mc] != 0;
     if (sel) {
       tok = arg;
       still = false;
-      a.tokens[cell] = arg;
-      a.masked[cell] = 0;
+      a.tokens[tc] = arg;
+      a.masked[mc] = 0;
     }
+  }
+  if (j < a.L) {
     if (a.conf_out) a.conf_out[cell] = m ? conf : -1.0f;
+    if (a.pos_out) a.pos_out[cell] = inb ? q.s + j : -1;
   }
   const bool e = inb && !still && a.eos_id >= 0 && tok == a.eos_id;
   const unsigned long long be = __ballot(e);
@@ -218,8 +229,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   static_assert(kDecPartChunks >= 1 && kDecPartChunks <= 4, "stream_part is instantiated for 1..4 chunks");
   const int row = blockIdx.x / a.parts, part = blockIdx.x - row * a.parts;
   const int i = row / a.L, j = row - i * a.L;
-  const Geo q = geo_of(a.reqs[i], a.L);
-  if (j >= q.B || a.masked[row] == 0) return;
+  const bs_req_desc rq = a.reqs[i];
+  const Geo q = geo_of(rq, a.L);
+  if (j >= q.B || a.masked[state_cell(a, rq, q, i, j, a.msk_rs)] == 0) return;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const T* x = static_cast<const T*>(a.logits) + (int64_t)row * a.row_stride;
   const int nchunk = (a.V + CH - 1) / CH;
@@ -283,16 +295,22 @@ __global__ __launch_bounds__(64) void k_decode_select(DecArgs a) {
 
 }  // namespace
 
-hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s) {
+hipError_t launch_decode_rows(const DecArgs& a, bs_dtype dt, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.n * a.L * a.parts)), block(kThreads);
   if (dt == BS_BF16)
     hipLaunchKernelGGL(k_decode_parts<uint16_t>, grid, block, 0, s, a);
   else
     hipLaunchKernelGGL(k_decode_parts<float>, grid, block, 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_select(const DecArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_decode_select, dim3(a.n), dim3(64), 0, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s) {
+  return launch_decode_marked(a, dt, s, [](int) { return hipSuccess; });
 }
 
 }  // namespace bs

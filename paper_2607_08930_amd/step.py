@@ -3,9 +3,12 @@
 Order (Algorithm 1's block-cycle, one denoising step): gather the active
 blocks' token ids and mask bits -> dual-cache block attention for each layer
 (with the in-place fresh-KV write) -> parallel decode -> scatter tokens and
-mask back into the dense box. At a block boundary ``compact`` first rewrites
-the KV boxes of every layer. PyTorch only provides device memory and the
-stream; every step runs in libblockserve's kernels.
+mask back into the dense box. ``run_step`` enqueues the whole step with one
+``bs_mixed_state_step`` call (decode then reads and writes the dense boxes
+directly) or, with ``fused=False``, as the separate K1/K2/K3/K1^-1 calls. At a
+block boundary ``compact`` first rewrites the KV boxes of every layer.
+PyTorch only provides device memory and the stream; every step runs in
+libblockserve's kernels.
 """
 from __future__ import annotations
 
@@ -15,7 +18,7 @@ import numpy as np
 import torch
 
 from . import (BS_BF16, BS_F32, Context, bs_decode_workspace_bytes, bs_dual_cache_block_attention,
-               bs_gather_active_blocks_n, bs_kv_scatter_compact, bs_parallel_decode,
+               bs_gather_active_blocks_n, bs_kv_scatter_compact, bs_mixed_state_step, bs_parallel_decode,
                bs_scatter_active_blocks_n)
 
 
@@ -98,21 +101,33 @@ class StepState:
 
 
 def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want_conf=False,
-             layers=None) -> None:
-    """Enqueue one step for the requests ``reqs`` (REQ_DTYPE, n <= n_max)."""
-    n = len(reqs)
+             layers=None, fused=True) -> None:
+    """Enqueue one step for the requests ``reqs`` (REQ_DTYPE, n <= n_max).
+
+    fused: one library call; the compact tok_c/msk_c are then not written.
+    pos is written either way."""
     L, R, W = st.L, st.R, st.W
     dt = dt_code(st.dtype)
+    lays = st.layers if layers is None else layers
+    conf = st.conf if want_conf else None
+    if fused:
+        bs_mixed_state_step(ctx, reqs, L, R, W,
+                            [(x.q, x.k_new, x.v_new, x.k_cache, x.v_cache, x.out) for x in lays],
+                            st.Hq, st.Hkv, st.D, dt, st.scale, st.write_back, st.V, dt, st.logits,
+                            st.logits.stride(1), st.tokens, st.tokens.stride(0), st.mask, st.mask.stride(0),
+                            st.tau, st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, conf, st.pos,
+                            st.dec_ws, st.dec_ws.numel(), stream=stream)
+        return
     strides = [st.tokens.stride(0) * 4, st.mask.stride(0)]
     bs_gather_active_blocks_n(ctx, reqs, L, R, W, [st.tokens, st.mask], strides, [4, 1], [st.tok_c, st.msk_c],
                               st.pos, stream=stream)
-    for lay in (st.layers if layers is None else layers):
+    for lay in lays:
         bs_dual_cache_block_attention(ctx, reqs, L, st.Hq, st.Hkv, st.D, dt, st.scale, lay.q, lay.k_new,
                                       lay.v_new, lay.k_cache, lay.v_cache, R, W, st.write_back, lay.out,
                                       None, 0, stream=stream)
     bs_parallel_decode(ctx, reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c, st.tau,
-                       st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen,
-                       st.conf if want_conf else None, st.dec_ws, st.dec_ws.numel(), stream=stream)
+                       st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, conf, st.dec_ws,
+                       st.dec_ws.numel(), stream=stream)
     bs_scatter_active_blocks_n(ctx, reqs, L, R, W, [st.tok_c, st.msk_c], [4, 1], [st.tokens, st.mask], strides,
                                stream=stream)
 

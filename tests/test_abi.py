@@ -64,6 +64,10 @@ def test_calls_without_context_fail_before_any_device_work():
                                      None, None, None, 0, None) == 1
     assert bs.lib.bs_kv_scatter_compact(null, None, 0, 1, 1, 8, 0, None, None, 0, 1, 1, None, None, 0, 1, 1,
                                         None, None, 0, 1, 1, None) == 1
+    assert bs.lib.bs_mixed_state_step(null, None, 0, 8, 1, 1, 0, 1, 1, 64, 0, 0.0, 1, None, None, None, None,
+                                      None, None, 10, 0, None, 16, None, 1, None, 1, 0.9, 1, -1, None, None,
+                                      None, None, None, None, 0, None) == 1
+    assert bs.lib.bs_profile_begin(null, 4) == 1
     assert "ctx is NULL" in bs.bs_last_error()
 
 

@@ -135,6 +135,19 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a, int jblocks) {
 // drain every stage in flight before reading the current one.
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// max without the canonicalisation fmaxf needs in IEEE mode (scores are finite
+// or -inf, so NaN propagation never applies)
+__device__ inline float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
+
+// lsum += sum of the eight bf16 weights in p (the values the P V MFMA uses)
+__device__ inline float add_weights(float lsum, const bf16x8_t& p) {
+  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) lsum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{p[2 * k], p[2 * k + 1]}, one, lsum, false);
+  return lsum;
+}
 typedef __attribute__((address_space(3))) void lds_void;
 
 // XOR swizzle of a row's 16-byte slots. Rows r0..r0+3 (r0 % 4 == 0) differ in
@@ -169,16 +182,26 @@ __device__ inline void dma16_sv(uint32_t lds, uint64_t base, uint32_t off) {
                : "memory");
 }
 
-// Wait until at most n of this wave's vector-memory operations are outstanding.
+// Wait until at most N (compile time) / n (run time, wave-uniform) of this
+// wave's vector-memory operations are outstanding. gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]; counts above 63
+// wait for everything.
+template <int N>
+__device__ inline void wait_vm_c() {
+  constexpr int n = N > 63 ? 0 : N;
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 __device__ inline void wait_vm(int n) {
-  // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
-#define BS_VM(N) case N: __builtin_amdgcn_s_waitcnt(((N) & 15) | (((N) >> 4) << 14) | (7 << 4) | (15 << 8)); break;
+#define BS_VM(N) case N: wait_vm_c<N>(); break;
   switch (n) {
-    BS_VM(0) BS_VM(1) BS_VM(2) BS_VM(3) BS_VM(4) BS_VM(5) BS_VM(6) BS_VM(7) BS_VM(8) BS_VM(9) BS_VM(10)
-    BS_VM(11) BS_VM(12) BS_VM(13) BS_VM(14) BS_VM(15) BS_VM(16) BS_VM(17) BS_VM(18) BS_VM(19) BS_VM(20)
-    BS_VM(21) BS_VM(22) BS_VM(23) BS_VM(24) BS_VM(25) BS_VM(26) BS_VM(27) BS_VM(28) BS_VM(29) BS_VM(30)
-    BS_VM(31) BS_VM(32)
-    default: __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); break;
+    BS_VM(0) BS_VM(1) BS_VM(2) BS_VM(3) BS_VM(4) BS_VM(5) BS_VM(6) BS_VM(7) BS_VM(8) BS_VM(9)
+     BS_VM(10) BS_VM(11) BS_VM(12) BS_VM(13) BS_VM(14) BS_VM(15) BS_VM(16) BS_VM(17) BS_VM(18) BS_VM(19)
+     BS_VM(20) BS_VM(21) BS_VM(22) BS_VM(23) BS_VM(24) BS_VM(25) BS_VM(26) BS_VM(27) BS_VM(28) BS_VM(29)
+     BS_VM(30) BS_VM(31) BS_VM(32) BS_VM(33) BS_VM(34) BS_VM(35) BS_VM(36) BS_VM(37) BS_VM(38) BS_VM(39)
+     BS_VM(40) BS_VM(41) BS_VM(42) BS_VM(43) BS_VM(44) BS_VM(45) BS_VM(46) BS_VM(47) BS_VM(48) BS_VM(49)
+     BS_VM(50) BS_VM(51) BS_VM(52) BS_VM(53) BS_VM(54) BS_VM(55) BS_VM(56) BS_VM(57) BS_VM(58) BS_VM(59)
+     BS_VM(60) BS_VM(61) BS_VM(62) BS_VM(63)
+    default: wait_vm_c<0>(); break;
   }
 #undef BS_VM
 }
@@ -295,40 +318,78 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) o[dt][rr] = 0.0f;
   float mrun = -__builtin_inff(), lsum = 0.0f;
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int nxt = tile + NS - 1;
-    if (nxt < ntiles) issue(nxt % NS, nxt * KT);
-    // this tile's stage has landed once only the later stages' DMAs remain
-    wait_vm(nblk * (min(ntiles, tile + NS) - tile - 1));
-    if constexpr (SHARED) __syncthreads();
-    const uint16_t* kt = ring + (tile % NS) * STAGE;
-    const uint16_t* vtl = kt + TILE;
-    const int tb = tile * KT;
+  if constexpr (SHARED) {
+    static_assert(KT == 64 && NS >= 3, "the pipelined group loop keeps two 64-key tiles resident");
+    // Software pipeline: iteration t turns tile t's scores (computed in
+    // iteration t - 1) into probabilities and accumulates P V while the score
+    // MFMAs of tile t + 1 run, so the VALU and matrix pipes overlap inside the
+    // wave. Tiles t and t + 1 are resident; t + 2 .. t + NS - 1 are in flight.
+    auto scores = [&](const uint16_t* kt, f32x16_t& s0, f32x16_t& s1) {
 #pragma unroll
-    for (int sub = 0; sub < KT / 32; ++sub) {
-      const int sb = tb + sub * 32;
-      if (sb >= len) break;
-      f32x16_t sacc;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) sacc[rr] = 0.0f;
+      for (int rr = 0; rr < 16; ++rr) {
+        s0[rr] = 0.0f;
+        s1[rr] = 0.0f;
+      }
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kt + sub * 32 * D + koff[kk]);
-        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[kk], sacc, 0, 0, 0);
+        const bf16x8_t k0 = *reinterpret_cast<const bf16x8_t*>(kt + koff[kk]);
+        const bf16x8_t k1 = *reinterpret_cast<const bf16x8_t*>(kt + 32 * D + koff[kk]);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[kk], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[kk], s1, 0, 0, 0);
       }
-      // lane (g, n) holds S^T[key 8 (rr / 4) + 4 g + rr % 4][query n] (unscaled)
-      if (sb + 32 > len) {                       // ragged last sub-tile only
+    };
+    auto probs = [&](const f32x16_t& sc, bf16x8_t& p0, bf16x8_t& p1) {
+      const float nm = -mrun;
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr)
-          if (sb + 8 * (rr >> 2) + 4 * g + (rr & 3) >= len) sacc[rr] = -__builtin_inff();
+      for (int rr = 0; rr < 16; ++rr) {
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[rr], a.scale_log2e, nm));
+        if (rr < 8)
+          p0[rr] = (__bf16)pv;
+        else
+          p1[rr - 8] = (__bf16)pv;
       }
-      float mx = sacc[0];
+      lsum = add_weights(add_weights(lsum, p0), p1);
+    };
+    auto pv = [&](const uint16_t* vs, const bf16x8_t& p0, const bf16x8_t& p1) {
 #pragma unroll
-      for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, sacc[rr]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
-      // lazy rescale: keep the reference max until a score exceeds it by 2^8,
-      // so the O accumulators are rescaled a handful of times per row
-      if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
+          const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
+          const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ks ? p1 : p0, o[dt], 0, 0, 0);
+        }
+    };
+
+    // tile 0 resident (the later prologue stages may still be in flight)
+    wait_vm(nblk * min(ntiles - 1, NS - 2));
+    __syncthreads();
+    f32x16_t sa, sb;
+    scores(ring, sa, sb);
+    for (int tile = 0; tile < ntiles; ++tile) {
+      if (tile + 1 < ntiles) {
+        // tile + 1 landed (stages up to tile + NS - 2 were issued); after the
+        // barrier every wave is done with tile - 1, whose slot is refilled
+        wait_vm(nblk * max(0, min(ntiles - 1, tile + NS - 2) - tile - 1));
+        __syncthreads();
+        const int nxt = tile + NS - 1;
+        if (nxt < ntiles) issue(nxt % NS, nxt * KT);
+      }
+      const int tb = tile * KT;
+      if (tb + KT > len) {                         // ragged last tile only
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int key = tb + 8 * (rr >> 2) + 4 * g + (rr & 3);
+          if (key >= len) sa[rr] = -__builtin_inff();
+          if (key + 32 >= len) sb[rr] = -__builtin_inff();
+        }
+      }
+      float mx = vmax(sa[0], sb[0]);
+#pragma unroll
+      for (int rr = 1; rr < 16; ++rr) mx = vmax(mx, vmax(sa[rr], sb[rr]));
+      mx = vmax(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
+      if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {         // lazy rescale, as below
         const float mnew = fmaxf(mrun, mx);
         const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
         lsum *= alpha;
@@ -338,31 +399,88 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
           for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
         mrun = mnew;
       }
-      bf16x8_t pb0, pb1;
-      const float nm = -mrun;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[rr], a.scale_log2e, nm));
-        lsum += p;
-        if (rr < 8)
-          pb0[rr] = (__bf16)p;
-        else
-          pb1[rr - 8] = (__bf16)p;
-      }
-      const uint16_t* vs = vtl + sub * 32 * D;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
-          const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
-          const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ks ? pb1 : pb0, o[dt], 0, 0, 0);
-        }
+      bf16x8_t pa0, pa1, pb0, pb1;
+      probs(sa, pa0, pa1);
+      probs(sb, pb0, pb1);
+      // scores of tile + 1 (on the last tile they read a resident slot and are
+      // discarded), independent of the probabilities above
+      scores(ring + ((tile + 1) % NS) * STAGE, sa, sb);
+      const uint16_t* vt = ring + (tile % NS) * STAGE + TILE;
+      pv(vt, pa0, pa1);
+      pv(vt + 32 * D, pb0, pb1);
     }
-    // the stage is refilled NS - 1 tiles later: every reader must be done
-    // (a single wave consumed its LDS reads through the MFMAs above)
-    if constexpr (SHARED) __syncthreads();
+  } else {
+    for (int tile = 0; tile < ntiles; ++tile) {
+      const int nxt = tile + NS - 1;
+      if (nxt < ntiles) issue(nxt % NS, nxt * KT);
+      // this tile's stage has landed once only the later stages' DMAs remain
+      // (a single wave issues all 2 * BPT blocks of a stage)
+      if (tile + NS <= ntiles)
+        wait_vm_c<2 * BPT * (NS - 1)>();
+      else
+        wait_vm(nblk * (ntiles - tile - 1));
+      const uint16_t* kt = ring + (tile % NS) * STAGE;
+      const uint16_t* vtl = kt + TILE;
+      const int tb = tile * KT;
+  #pragma unroll
+      for (int sub = 0; sub < KT / 32; ++sub) {
+        const int sb = tb + sub * 32;
+        if (sb >= len) break;
+        f32x16_t sacc;
+  #pragma unroll
+        for (int rr = 0; rr < 16; ++rr) sacc[rr] = 0.0f;
+  #pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) {
+          const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kt + sub * 32 * D + koff[kk]);
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[kk], sacc, 0, 0, 0);
+        }
+        // lane (g, n) holds S^T[key 8 (rr / 4) + 4 g + rr % 4][query n] (unscaled)
+        if (sb + 32 > len) {                       // ragged last sub-tile only
+  #pragma unroll
+          for (int rr = 0; rr < 16; ++rr)
+            if (sb + 8 * (rr >> 2) + 4 * g + (rr & 3) >= len) sacc[rr] = -__builtin_inff();
+        }
+        float mx = sacc[0];
+#pragma unroll
+        for (int rr = 1; rr < 16; ++rr) mx = vmax(mx, sacc[rr]);
+        mx = vmax(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
+        // lazy rescale: keep the reference max until a score exceeds it by 2^8,
+        // so the O accumulators are rescaled a handful of times per row
+        if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {
+          const float mnew = fmaxf(mrun, mx);
+          const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
+          lsum *= alpha;
+  #pragma unroll
+          for (int dt = 0; dt < NDT; ++dt)
+  #pragma unroll
+            for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
+          mrun = mnew;
+        }
+        bf16x8_t pb0, pb1;
+        const float nm = -mrun;
+  #pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[rr], a.scale_log2e, nm));
+          if (rr < 8)
+            pb0[rr] = (__bf16)p;
+          else
+            pb1[rr - 8] = (__bf16)p;
+        }
+        lsum = add_weights(add_weights(lsum, pb0), pb1);
+        const uint16_t* vs = vtl + sub * 32 * D;
+  #pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+  #pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
+            const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
+            const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ks ? pb1 : pb0, o[dt], 0, 0, 0);
+          }
+      }
+      // the wave consumed its LDS reads through the MFMAs above before its
+      // next issue overwrites the slot
+    }
   }
   const float lt = lsum + __shfl_xor(lsum, 32, 64);
   // in-place KV update: the group's waves store the fresh block rows of this
@@ -414,16 +532,16 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
 }
 
 // One query head per KV head and at most 32 block rows (MHA with L <= 32):
-// four independent waves per workgroup, each owning one item and an NS-stage
+// NW independent waves per workgroup, each owning one item and an NS-stage
 // ring of 32-key tiles.
-template <int D, int NS>
-__global__ __launch_bounds__(256, 1) void k_attn_bf16_wave(AttnArgs a) {
+template <int D, int NS, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void k_attn_bf16_wave(AttnArgs a) {
   constexpr int STAGE = 2 * 32 * D;
-  __shared__ __align__(1024) uint16_t lds[4 * NS * STAGE];
+  __shared__ __align__(1024) uint16_t lds[NW * NS * STAGE];
   // the wave index is wave-uniform: through readfirstlane every quantity
   // derived from it (item, DMA block, base pointers) lives in SGPRs
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int idx = blockIdx.x * 4 + w;
+  const int idx = blockIdx.x * NW + w;
   if (idx >= a.n_items) return;
   attn_item<D, 32, NS, false, 2 * (32 * D / 512)>(a, a.items[idx], lds + w * NS * STAGE, 1, 0, threadIdx.x & 63);
 }
@@ -442,11 +560,12 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
 template <int D>
 hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   if (GW == 1) {
-    hipLaunchKernelGGL((k_attn_bf16_wave<D, 2>), dim3((a.n_items + 3) / 4), dim3(256), 0, s, a);
+    constexpr int NS = 2, NW = 4;
+    hipLaunchKernelGGL((k_attn_bf16_wave<D, NS, NW>), dim3((a.n_items + NW - 1) / NW), dim3(64 * NW), 0, s, a);
   } else if (GW <= 4) {
-    hipLaunchKernelGGL((k_attn_bf16_group<D, 3, 2>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
+    hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 2>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_attn_bf16_group<D, 3, 5>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
+    hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 5>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   }
   return hipGetLastError();
 }

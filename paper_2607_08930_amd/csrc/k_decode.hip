@@ -25,9 +25,13 @@ constexpr int kThreads = 256;
 constexpr int kLoads = kDecChunkBytes / (kThreads * 16);  // 8
 constexpr float kLog2e = 1.4426950408889634f;
 
+// max without the canonicalisation fmaxf needs in IEEE mode: every value
+// reduced here is a finite logit or -inf (masked tail), never NaN
+__device__ inline float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
+
 __device__ inline float wave_max(float v) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  for (int o = 32; o >= 1; o >>= 1) v = vmax(v, __shfl_xor(v, o, 64));
   return v;
 }
 __device__ inline float wave_sum(float v) {
@@ -114,7 +118,7 @@ __device__ inline void fold_vector(const v4u& v, int e0, RowAcc& r) {
   for (int k = 0; k < N; ++k) f[k] = Lanes<T>::get(v, k);
   float vm = f[0];
 #pragma unroll
-  for (int k = 1; k < N; ++k) vm = fmaxf(vm, f[k]);
+  for (int k = 1; k < N; ++k) vm = vmax(vm, f[k]);
   if (vm > r.mt) {
     r.mt = vm;
     r.vbest = e0;
@@ -147,26 +151,41 @@ __device__ inline int64_t state_cell(const DecArgs& a, const bs_req_desc& r, con
 }
 
 __device__ inline void select_request(const DecArgs& a, int i, int lane) {
-  const bs_req_desc rq = a.reqs[i];
-  const Geo q = geo_of(rq, a.L);
   const int j = lane;
   const int64_t cell = (int64_t)i * a.L + j;   // compact index: logits rows, part results, conf_out
+  // The part results do not depend on the descriptor: their loads are issued
+  // first so that they travel together with the descriptor's.
+  constexpr int kUnroll = 8;
+  const DecPartial* pp = a.part + (j < a.L ? cell : (int64_t)i * a.L) * a.parts;
+  DecPartial pr[kUnroll];
+#pragma unroll
+  for (int p = 0; p < kUnroll; ++p) pr[p] = pp[min(p, a.parts - 1)];
+  const bs_req_desc rq = a.reqs[i];
+  const Geo q = geo_of(rq, a.L);
   const bool inb = j < q.B;
   const int64_t tc = inb ? state_cell(a, rq, q, i, j, a.tok_rs) : 0;
   const int64_t mc = inb ? state_cell(a, rq, q, i, j, a.msk_rs) : 0;
+  const int tok0 = inb ? a.tokens[tc] : 0;
   const bool m = inb && a.masked[mc] != 0;
   float conf = -1.0f;
   int arg = 0;
   if (m) {
-    const DecPartial* pp = a.part + cell * a.parts;
     float M = -__builtin_inff();
-    for (int p = 0; p < a.parts; ++p) M = fmaxf(M, pp[p].m);
+#pragma unroll
+    for (int p = 0; p < kUnroll; ++p) M = fmaxf(M, pr[p].m);   // repeats of the last part change nothing
+    for (int p = kUnroll; p < a.parts; ++p) M = fmaxf(M, pp[p].m);
     float S = 0.0f;
     int A = INT_MAX;
-    for (int p = 0; p < a.parts; ++p) {
-      const DecPartial pr = pp[p];
-      S += pr.s * __builtin_amdgcn_exp2f((pr.m - M) * kLog2e);
-      if (pr.m == M) A = min(A, pr.a);
+#pragma unroll
+    for (int p = 0; p < kUnroll; ++p)
+      if (p < a.parts) {
+        S += pr[p].s * __builtin_amdgcn_exp2f((pr[p].m - M) * kLog2e);
+        if (pr[p].m == M) A = min(A, pr[p].a);
+      }
+    for (int p = kUnroll; p < a.parts; ++p) {
+      const DecPartial x = pp[p];
+      S += x.s * __builtin_amdgcn_exp2f((x.m - M) * kLog2e);
+      if (x.m == M) A = min(A, x.a);
     }
     conf = 1.0f / S;
     arg = A;
@@ -177,23 +196,22 @@ __device__ inline void select_request(const DecArgs& a, int i, int lane) {
   const int nT = __popcll(bt);
   const int nsel = min(nM, max(a.q_min, nT));
   // rank among masked positions: higher confidence first, then smaller j
+  // (lane jj's confidence is read through the scalar unit)
   int rank = 0;
-  for (int jj = 0; jj < 64; ++jj) {
-    const float cj = __shfl(conf, jj, 64);
-    if (((bm >> jj) & 1ull) && (cj > conf || (cj == conf && jj < j))) ++rank;
+  const int cbits = __float_as_int(conf);
+  for (unsigned long long rest = bm; rest; rest &= rest - 1) {
+    const int jj = __builtin_ctzll(rest);
+    const float cj = __int_as_float(__builtin_amdgcn_readlane(cbits, jj));
+    if (cj > conf || (cj == conf && jj < j)) ++rank;
   }
   const bool sel = m && rank < nsel;
-  int tok = 0;
-  bool still = false;
-  if (inb) {
-    tok = a.tokens[tc];
-    still = a.masked[mc] != 0;
-    if (sel) {
-      tok = arg;
-      still = false;
-      a.tokens[tc] = arg;
-      a.masked[mc] = 0;
-    }
+  int tok = tok0;
+  bool still = m;
+  if (sel) {
+    tok = arg;
+    still = false;
+    a.tokens[tc] = arg;
+    a.masked[mc] = 0;
   }
   if (j < a.L) {
     if (a.conf_out) a.conf_out[cell] = m ? conf : -1.0f;
@@ -254,7 +272,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   __syncthreads();
   float M = sm[0];
 #pragma unroll
-  for (int k = 1; k < kThreads / 64; ++k) M = fmaxf(M, sm[k]);
+  for (int k = 1; k < kThreads / 64; ++k) M = vmax(M, sm[k]);
   // r.mb <= r.mt * log2 e <= M * log2 e, so the factor is at most 1
   const float sc = r.s * __builtin_amdgcn_exp2f(r.mb - M * kLog2e);
   // smallest index holding M: threads whose max is M re-read the one vector

@@ -100,6 +100,86 @@ def cpu_baseline(w, host, budget_s=12.0, max_reps=200):
                       f"{w.layers} layer(s) each), fp64 NumPy, {el:.1f} s"}
 
 
+KERNEL_SOURCES = {   # kernel name prefix -> sources whose change voids its counter-derived traffic
+    "k_attn_bf16": ["k_attention.hip", "bs_internal.h"],
+    "k_attn_f32": ["k_attention.hip", "bs_internal.h"],
+    "k_decode_parts": ["k_decode.hip", "bs_internal.h"],
+    "k_decode_select": ["k_decode.hip", "bs_internal.h"],
+}
+CALIB_BYTES = 256 << 20          # the --pmc-calibration copy reads and writes this many bytes
+
+
+def source_hash(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[next(k for k in KERNEL_SOURCES if kernel.startswith(k))] + ["../build.py"]:
+        h.update(open(os.path.join(ROOT, "paper_2607_08930_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+
+
+def read_traffic(workload, kernel):
+    """Measured HBM bytes per launch of `kernel` from the committed counter
+    summary, or None when there is none or the kernel's sources changed since."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.strip().strip("`").split()
+        if len(f) == 4 and f[0] == "traffic" and kernel.startswith(f[1]) and f[3] == source_hash(f[1]):
+            return int(f[2])
+    return None
+
+
+def traffic_summary(args, workload):
+    """Counter CSVs of a FETCH_SIZE run and a WRITE_SIZE run -> profiles/traffic_<workload>.md.
+    Both counters are KiB per dispatch; each is scaled by what it reads for the
+    calibration copy of CALIB_BYTES."""
+    import csv
+    import glob
+
+    def load(d, counter):
+        per = {}
+        for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(fn)):
+                if r["Counter_Name"] == counter:
+                    per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return per
+
+    fetch, write = load(args.traffic_summary[0], "FETCH_SIZE"), load(args.traffic_summary[1], "WRITE_SIZE")
+    cal_f = max(v for k, vs in fetch.items() if "copyBuffer" in k for v in vs)
+    cal_w = max(v for k, vs in write.items() if "copyBuffer" in k for v in vs)
+    kf, kw = CALIB_BYTES / (cal_f * 1024), CALIB_BYTES / (cal_w * 1024)
+    lines = [f"# Measured HBM traffic per launch: {workload}", "",
+             "Commands (repo root as `$R`, one MI355X; the bench adds one 256 MiB device copy as the",
+             "calibration kernel):", "", "```", "cd /tmp && export TMPDIR=/tmp"]
+    for c, d in (("FETCH_SIZE", args.traffic_summary[0]), ("WRITE_SIZE", args.traffic_summary[1])):
+        lines.append(f"rocprofv3 --pmc {c} -d {d} -o run --output-format csv -- "
+                     f"python3 $R/bench.py --config {args.config} --steps 5 --warmup 1 --no-cpu-baseline --pmc-calibration")
+    lines += [f"python3 $R/bench.py --config {args.config} --traffic-summary <fetch dir> <write dir>", "```", "",
+              f"Calibration (256 MiB copy): FETCH_SIZE reads {cal_f:.0f} KiB (scale x{kf:.3f}), "
+              f"WRITE_SIZE reads {cal_w:.0f} KiB (scale x{kw:.3f}).", "",
+              "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | read bytes | written bytes | total bytes |",
+              "|---|---:|---:|---:|---:|---:|---:|"]
+    keep = []
+    for name in sorted(set(fetch) & set(write)):
+        short = name.replace("void ", "").replace("bs::(anonymous namespace)::", "").split("(")[0]
+        pref = next((k for k in KERNEL_SOURCES if short.startswith(k)), None)
+        if pref is None:
+            continue
+        f_ = float(np.mean(fetch[name])); w_ = float(np.mean(write[name]))
+        rd, wr = f_ * 1024 * kf, w_ * 1024 * kw
+        lines.append(f"| `{short}` | {len(fetch[name])} | {f_:.0f} | {w_:.0f} | {rd:.0f} | {wr:.0f} | {rd + wr:.0f} |")
+        keep.append(f"`traffic {pref} {int(round(rd + wr))} {source_hash(pref)}`")
+    lines += ["", "Machine-readable (kernel, bytes per launch, hash of the kernel's sources when measured;",
+              "bench.py reports `traffic` only while the hash matches):", ""] + [k + "  " for k in keep] + [""]
+    open(traffic_file(workload), "w").write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,7 +188,15 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="workload 1-4 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
+    ap.add_argument("--pmc-calibration", action="store_true",
+                    help="run one 256 MiB device copy first (the reference kernel for FETCH_SIZE / WRITE_SIZE)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs into profiles/traffic_<workload>.md (no GPU needed)")
     args = ap.parse_args()
+    if args.traffic_summary:
+        import synth
+        traffic_summary(args, synth.workload(args.config).name)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
               file=sys.stderr, flush=True)
@@ -133,6 +221,12 @@ def main():
     flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")    # 512 MiB, swept by reading
     stream = torch.cuda.current_stream()
     ctx = bs.Context(0)
+    if args.pmc_calibration:
+        src_ = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst_ = torch.empty_like(src_)
+        dst_.copy_(src_)
+        torch.cuda.synchronize()
+        del src_, dst_
 
     def one_step():
         bstep.run_step(ctx, st, w.reqs, stream=stream)
@@ -179,14 +273,17 @@ def main():
     dec_gbs = logits_bytes / (rows_ms / 1e3) / 1e9
     attn_dominant = ab["attn"] >= logits_bytes
     if attn_dominant:
-        roof = {"kernel": "k_attn_bf16_wave" if w.dtype == "bf16" else "k_attn_f32", "bound": "hbm",
+        gw = (w.Hq // w.Hkv) * ((w.L + 31) // 32)
+        roof = {"kernel": ("k_attn_bf16_wave" if gw == 1 else "k_attn_bf16_group") if w.dtype == "bf16" else "k_attn_f32",
+                "bound": "hbm",
                 "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                 "algorithmic_bytes_per_launch": ab["attn_per_layer"], "avg_launch_ms": round(attn_ms, 5)}
     else:
         roof = {"kernel": "k_decode_parts", "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                 "algorithmic_bytes_per_launch": logits_bytes, "avg_launch_ms": round(rows_ms, 5)}
+    roof["traffic"] = read_traffic(w.name, roof["kernel"])
     ctx.close()
     res = {
         "metric": "denoised block positions/s per mixed-state step",

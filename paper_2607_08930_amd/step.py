@@ -137,8 +137,14 @@ def compact(ctx: Context, segs: np.ndarray, n_layers: int, Hkv: int, D: int, dty
             dst_k: torch.Tensor, dst_v: torch.Tensor, stream=None) -> None:
     """KV boxes are [layers][R][Hkv][W][D] tensors; strides come from them."""
     eb = src_k.element_size()
-    bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt_code(dtype), src_k, src_v, src_k.stride(0) * eb,
+
+    def layer_stride(t):
+        # a unit layer axis may carry any stride (NumPy gives a new axis
+        # stride 0); with one layer the box size is the stride that matters
+        return t.stride(0) * eb if t.shape[0] > 1 else t[0].numel() * eb
+
+    bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt_code(dtype), src_k, src_v, layer_stride(src_k),
                           src_k.shape[1], src_k.shape[3], stg_k, stg_v,
-                          stg_k.stride(0) * eb if stg_k is not None else 0,
+                          layer_stride(stg_k) if stg_k is not None else 0,
                           stg_k.shape[1] if stg_k is not None else 1, stg_k.shape[3] if stg_k is not None else 1,
-                          dst_k, dst_v, dst_k.stride(0) * eb, dst_k.shape[1], dst_k.shape[3], stream=stream)
+                          dst_k, dst_v, layer_stride(dst_k), dst_k.shape[1], dst_k.shape[3], stream=stream)

@@ -113,28 +113,33 @@ def run_decode(ctx, w, logits, tok_c, msk_c, *, tau=None, q_min=None, eos_id=Non
                 done=done.cpu().numpy(), eos_seen=eos.cpu().numpy(), conf=conf.cpu().numpy(), ws=ws)
 
 
-def exempt_requests(ref, reqs, L, tau):
-    """Requests whose selection is not fixed at fp32 precision: a masked
-    confidence within EXEMPT of tau, or a near-tie (gap <= EXEMPT) between the
-    last selected and the first unselected confidence."""
+def exempt_requests(ref, reqs, L, tau, q_min=1):
+    """Requests whose selection is not fixed at fp32 precision: the number
+    selected changes when every confidence within EXEMPT of tau moves by
+    EXEMPT either way, or the last selected and first unselected confidences
+    are within EXEMPT of each other. (A confidence near tau that cannot change
+    the count -- e.g. when the quota q_min decides it -- exempts nothing.)"""
     ex = set()
     for i, r in enumerate(reqs):
         t = oracle.geometry(r, L)
         cs = sorted((ref["conf"][i, j] for j in range(t.B) if ref["conf"][i, j] >= 0), reverse=True)
         if not cs:
             continue
+        nm = len(cs)
+        n_lo = min(nm, max(q_min, sum(c >= tau + EXEMPT for c in cs)))
+        n_hi = min(nm, max(q_min, sum(c >= tau - EXEMPT for c in cs)))
         nsel = int(ref["n_unmasked"][i])
-        if any(abs(c - tau) <= EXEMPT for c in cs):
+        if n_lo != n_hi:
             ex.add(i)
-        elif 0 < nsel < len(cs) and cs[nsel - 1] - cs[nsel] <= EXEMPT:
+        elif 0 < nsel < nm and cs[nsel - 1] - cs[nsel] <= EXEMPT:
             ex.add(i)
     return ex
 
 
-def check_decode(w, got, ref, reqs=None, tau=None, label=""):
+def check_decode(w, got, ref, reqs=None, tau=None, label="", q_min=None):
     reqs = w.reqs if reqs is None else reqs
     tau = w.tau if tau is None else tau
-    ex = exempt_requests(ref, reqs, w.L, tau)
+    ex = exempt_requests(ref, reqs, w.L, tau, w.q_min if q_min is None else q_min)
     for i, r in enumerate(reqs):
         t = oracle.geometry(r, w.L)
         m = ref["conf"][i] >= 0

@@ -119,7 +119,7 @@ def _decode_case(ctx, w, label, tau=None, q_min=None, eos_id=None):
     ref = oracle.parallel_decode(w.reqs, w.L, logits, tok_c, msk_c, tau=w.tau if tau is None else tau,
                                  q_min=w.q_min if q_min is None else q_min,
                                  eos_id=w.eos_id if eos_id is None else eos_id, dtype=w.dtype)
-    nex = check_decode(w, got, ref, tau=tau, label=label)
+    nex = check_decode(w, got, ref, tau=tau, label=label, q_min=q_min)
     say(f"  exempt requests: {nex} of {w.n}")
     return got, ref, nex
 

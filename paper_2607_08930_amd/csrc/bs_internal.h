@@ -62,6 +62,8 @@ struct AttnArgs {
   int write_back;
 };
 
+constexpr int kMhaWaves = 4;  // waves (independent items) per workgroup of the single-wave bf16 kernel
+
 hipError_t launch_attn_f32(const AttnArgs& a, int n_req, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s);
 

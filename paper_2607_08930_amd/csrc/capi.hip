@@ -250,9 +250,11 @@ int check_attention_tensors(bs_ctx* c, const void* q, const void* k_new, const v
 }
 
 // Descriptors, then (bf16) the (request, KV head) work items, longest rows
-// first: neighbours in a workgroup have similar lengths and the tail of the
-// grid is made of short items.
-void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hkv, bs_dtype dt) {
+// first, so the tail of the grid is made of short items. When one wave owns
+// an item (G = 1, L <= 32), workgroup b takes the items ranked b, b + NB,
+// b + 2 NB, ... (NB workgroups): every CU streams about the same number of
+// bytes instead of some CUs getting only the longest rows.
+void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, bs_dtype dt) {
   blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
   if (dt == BS_BF16) {
     std::vector<AttnItem> items;
@@ -262,6 +264,14 @@ void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hkv, 
       for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, 0});
     }
     std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
+    const size_t N = items.size();
+    if (Hq == Hkv && L <= 32 && N % kMhaWaves == 0) {
+      const size_t NB = N / kMhaWaves;
+      std::vector<AttnItem> mixed(N);
+      for (size_t b = 0; b < NB; ++b)
+        for (size_t j = 0; j < (size_t)kMhaWaves; ++j) mixed[b * kMhaWaves + j] = items[j * NB + b];
+      items.swap(mixed);
+    }
     blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * items.size());
     blob.meta[2] = (int)items.size();
   }
@@ -483,8 +493,8 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
-              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hkv, dt); }, &sl);
+  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
   if (st) return st;
   AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);
   a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
@@ -563,8 +573,8 @@ int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R,
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
-              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hkv, dt); }, &sl);
+  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
   if (st) return st;
   hipError_t e = prof_mark(c, 0, s);
   AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);

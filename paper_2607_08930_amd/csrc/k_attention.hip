@@ -560,7 +560,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
 template <int D>
 hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   if (GW == 1) {
-    constexpr int NS = 2, NW = 4;
+    constexpr int NS = 2, NW = kMhaWaves;
     hipLaunchKernelGGL((k_attn_bf16_wave<D, NS, NW>), dim3((a.n_items + NW - 1) / NW), dim3(64 * NW), 0, s, a);
   } else if (GW <= 4) {
     hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 2>), dim3(a.n_items), dim3(64 * GW), 0, s, a);

@@ -267,6 +267,84 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
 int bs_profile_begin(bs_ctx* ctx, int max_steps);
 int bs_profile_end(bs_ctx* ctx, float* phase_ms, int max_steps, int* n_steps);
 
+/* ------------------------------------------------------------------------
+ * Host scheduler: block-grained scheduling (Algorithm 1) with compute-aware
+ * admission (Section "Compute-aware admission control", Eq. 1). Host memory
+ * only; it plans, the step entry points above execute. One block-cycle:
+ *   bs_sched_refill  -> descriptors of the active set (row order), the
+ *                       admitted requests and the K4 segments that copy their
+ *                       staged (prefilled) rows into the box;
+ *   the caller runs K4 and then denoising steps until every active block is
+ *   fully unmasked;
+ *   bs_sched_complete -> every active request advances one block; requests at
+ *                       K_i blocks or reporting EOS leave the active set.
+ * Queue order, sand filling and the Fixed variant follow the paper; where it
+ * is silent: the queue is ascending in p by default (ties: arrival order); a
+ * refill alternates two moves until neither admits anything: admit every
+ * sand-filling candidate (p + L no wider than the current box) whose
+ * admission keeps Eq. 1 within the budget, scanning the whole queue, then
+ * admit the head of the queue if it fits (it may widen the box); the Fixed
+ * policy admits from the head while fewer than fixed_batch are active. Eq. 1
+ * gates admissions only: the rows of admitted requests grow by L per block
+ * afterwards, as in Algorithm 1. An admitted request takes
+ * the lowest free row, right-aligned at off = width - (p + g).
+ * Errors: status codes as above; the detail is in bs_sched_last_error()
+ * (thread-local). Not thread-safe per scheduler.
+ * ---------------------------------------------------------------------- */
+typedef struct bs_sched bs_sched;
+
+enum { BS_SCHED_BUDGET = 0, BS_SCHED_FIXED = 1 };
+enum { BS_ORDER_ASCENDING = 0, BS_ORDER_DESCENDING = 1, BS_ORDER_ARRIVAL = 2 };
+
+typedef struct {
+  int32_t L;            /* block length */
+  int32_t policy;       /* BS_SCHED_BUDGET (Eq. 1 token budget) or BS_SCHED_FIXED (batch cap) */
+  int64_t budget;       /* Eq. 1 budget in tokens (budget policy) */
+  int32_t fixed_batch;  /* active-set cap (fixed policy) */
+  int32_t rows;         /* rows of the physical box (R) */
+  int32_t width;        /* columns of the physical box (W) */
+  int32_t order;        /* BS_ORDER_*: pending-queue order */
+} bs_sched_config;
+
+typedef struct {
+  int32_t id;  /* caller's request id (reported back) */
+  int32_t p;   /* prompt length */
+  int32_t g;   /* generation length */
+} bs_sched_request;
+
+/* Filled by bs_sched_refill; the arrays belong to the scheduler and stay valid
+ * until its next refill or destroy. */
+typedef struct {
+  int32_t n_active;             /* active requests after the refill */
+  const bs_req_desc* descs;     /* [n_active] descriptors in row order (k = block index) */
+  const int32_t* ids;           /* [n_active] request ids, same order */
+  int32_t n_admitted;           /* requests admitted by this refill */
+  const int32_t* admitted_ids;  /* [n_admitted] in admission order */
+  const bs_copy_seg* segs;      /* [n_admitted] staging row a (the a-th admitted request's
+                                   prefilled row, left-aligned) -> its row in the box */
+  int64_t cost;                 /* Eq. 1 of the active set */
+  int32_t box_width;            /* max over the active set of p + (b + 1) L */
+} bs_sched_plan;
+
+int bs_sched_create(bs_sched** out, const bs_sched_config* cfg);
+int bs_sched_destroy(bs_sched* s);
+/* Adds requests to the pending queue. Rejects (BS_ERR_DESCRIPTOR, nothing
+ * added) p < 0, g < 1, p + g > width, and under the budget policy p + L >
+ * budget (a request that could never be admitted). */
+int bs_sched_submit(bs_sched* s, const bs_sched_request* reqs, int n);
+int bs_sched_refill(bs_sched* s, bs_sched_plan* plan);
+/* End of a block-cycle. eos[i] (may be NULL) flags CheckEOS for the i-th
+ * request of the last plan's row order; n must equal the active count.
+ * evicted_ids ([n] capacity) receives the ids that left, *n_evicted their
+ * number. */
+int bs_sched_complete(bs_sched* s, const uint8_t* eos, int n, int32_t* evicted_ids, int32_t* n_evicted);
+/* Counters: pending, active, finished, completed block-cycles and the sum of
+ * active counts over them (Eq. 2: R = sum_active / (cycles * B)). Any output
+ * may be NULL. */
+int bs_sched_counts(const bs_sched* s, int32_t* n_pending, int32_t* n_active, int64_t* n_finished,
+                    int64_t* cycles, int64_t* sum_active);
+const char* bs_sched_last_error(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,6 +19,9 @@ geometry   block decomposition K_i = ceil(g_i / L) and block index
            execution"); effective compute ratio R (Eq. 2).
 gather     gather of each request's active block into a compact tensor and the
            inverse scatter (paragraph "Vectorized mixed-schedule execution").
+schedule   block-grained scheduling (Algorithm 1) and compute-aware admission
+           (Eq. 1, sand filling, Fixed variant, Section "Compute-aware
+           admission control"); effective compute ratio (Eq. 2).
 attention  block attention of the active block against the request's dual
            cache (cached prefix + fresh block + cached masked suffix), with the
            in-place write of the fresh block KV at its physical offsets
@@ -46,8 +49,10 @@ from .attention import dual_cache_block_attention, attention_rows
 from .decode import parallel_decode, row_stats
 from .compact import kv_scatter_compact
 from .step import mixed_state_step
+from . import schedule
 
 __all__ = [
+    "schedule",
     "geometry", "validate_reqs", "bbox_cost", "position_ids", "transfer_schedule",
     "effective_compute_ratio", "widen", "gather_active_blocks", "scatter_active_blocks",
     "dual_cache_block_attention", "attention_rows", "parallel_decode", "row_stats",

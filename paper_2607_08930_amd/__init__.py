@@ -22,6 +22,8 @@ __all__ = [
     "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
     "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_gather_active_blocks_n",
     "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_profile_begin", "bs_profile_end",
+    "bs_sched_create", "bs_sched_destroy", "bs_sched_submit", "bs_sched_refill", "bs_sched_complete",
+    "bs_sched_counts", "bs_sched_last_error", "Scheduler",
     "bs_attention_workspace_bytes",
     "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
     "bs_kv_scatter_compact",
@@ -80,6 +82,14 @@ _SIGS = {
                                    _f32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "bs_profile_begin": (_i32, [_vp, _i32]),
     "bs_profile_end": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_i32)]),
+    "bs_sched_create": (_i32, [ctypes.POINTER(_vp), _vp]),
+    "bs_sched_destroy": (_i32, [_vp]),
+    "bs_sched_submit": (_i32, [_vp, _vp, _i32]),
+    "bs_sched_refill": (_i32, [_vp, _vp]),
+    "bs_sched_complete": (_i32, [_vp, _vp, _i32, _vp, ctypes.POINTER(_i32)]),
+    "bs_sched_counts": (_i32, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i64),
+                               ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
+    "bs_sched_last_error": (ctypes.c_char_p, []),
     "bs_attention_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "bs_dual_cache_block_attention": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                              _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
@@ -298,3 +308,117 @@ def bs_profile_end(ctx, max_steps: int) -> np.ndarray:
     n = _i32(0)
     _check(lib.bs_profile_end(_ptr(ctx), out.ctypes.data, max_steps, ctypes.byref(n)), ctx)
     return out[:n.value].copy()
+
+
+# ---------------------------------------------------------------- host scheduler
+SCHED_BUDGET, SCHED_FIXED = 0, 1
+ORDER_ASCENDING, ORDER_DESCENDING, ORDER_ARRIVAL = 0, 1, 2
+
+
+class _SchedConfig(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("policy", ctypes.c_int32), ("budget", ctypes.c_int64),
+                ("fixed_batch", ctypes.c_int32), ("rows", ctypes.c_int32), ("width", ctypes.c_int32),
+                ("order", ctypes.c_int32)]
+
+
+class _SchedPlan(ctypes.Structure):
+    _fields_ = [("n_active", ctypes.c_int32), ("descs", _vp), ("ids", _vp), ("n_admitted", ctypes.c_int32),
+                ("admitted_ids", _vp), ("segs", _vp), ("cost", ctypes.c_int64), ("box_width", ctypes.c_int32)]
+
+
+SCHED_REQ_DTYPE = np.dtype([("id", np.int32), ("p", np.int32), ("g", np.int32)])
+
+
+def _sched_check(st):
+    if st != 0:
+        raise BlockServeError(st, lib.bs_sched_last_error().decode())
+
+
+def _view(ptr, n, dtype):
+    if n == 0:
+        return np.zeros(0, dtype)
+    buf = (ctypes.c_char * (n * np.dtype(dtype).itemsize)).from_address(ptr)
+    return np.frombuffer(buf, dtype=dtype).copy()
+
+
+class Scheduler:
+    """Host block-grained scheduler (bs_sched_*); see include/blockserve.h."""
+
+    def __init__(self, L, *, policy=SCHED_BUDGET, budget=0, fixed_batch=0, rows=1, width=1,
+                 order=ORDER_ASCENDING):
+        cfg = _SchedConfig(L, policy, budget, fixed_batch, rows, width, order)
+        h = _vp()
+        _sched_check(lib.bs_sched_create(ctypes.byref(h), ctypes.byref(cfg)))
+        self.handle = h.value
+        self.L, self.rows, self.width = L, rows, width
+
+    def close(self):
+        if self.handle:
+            lib.bs_sched_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def submit(self, reqs):
+        """reqs: iterable of (id, p, g)."""
+        a = np.array([tuple(int(x) for x in r) for r in reqs], dtype=SCHED_REQ_DTYPE)
+        _sched_check(lib.bs_sched_submit(self.handle, a.ctypes.data if len(a) else None, len(a)))
+
+    def refill(self) -> dict:
+        plan = _SchedPlan()
+        _sched_check(lib.bs_sched_refill(self.handle, ctypes.byref(plan)))
+        return dict(descs=_view(plan.descs, plan.n_active, REQ_DTYPE),
+                    ids=_view(plan.ids, plan.n_active, np.int32),
+                    admitted=_view(plan.admitted_ids, plan.n_admitted, np.int32),
+                    segs=_view(plan.segs, plan.n_admitted, SEG_DTYPE),
+                    cost=int(plan.cost), box_width=int(plan.box_width))
+
+    def complete(self, eos=None) -> np.ndarray:
+        """eos: per-request flags in the last plan's row order (its length must
+        equal the active count), or None for no EOS."""
+        e = None if eos is None else np.ascontiguousarray(eos, dtype=np.uint8)
+        n = self.counts()["active"] if e is None else len(e)
+        out = np.zeros(max(n, 1), np.int32)
+        ne = _i32(0)
+        _sched_check(lib.bs_sched_complete(self.handle, e.ctypes.data if e is not None else None, n,
+                                           out.ctypes.data, ctypes.byref(ne)))
+        return out[:ne.value].copy()
+
+    def counts(self) -> dict:
+        a, b = _i32(0), _i32(0)
+        c, d, e = _i64(0), _i64(0), _i64(0)
+        _sched_check(lib.bs_sched_counts(self.handle, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c),
+                                         ctypes.byref(d), ctypes.byref(e)))
+        return dict(pending=a.value, active=b.value, finished=c.value, cycles=d.value, sum_active=e.value)
+
+
+def bs_sched_create(L, **kw) -> Scheduler:
+    return Scheduler(L, **kw)
+
+
+def bs_sched_destroy(s: Scheduler) -> None:
+    s.close()
+
+
+def bs_sched_submit(s: Scheduler, reqs) -> None:
+    s.submit(reqs)
+
+
+def bs_sched_refill(s: Scheduler) -> dict:
+    return s.refill()
+
+
+def bs_sched_complete(s: Scheduler, eos=None) -> np.ndarray:
+    return s.complete(eos)
+
+
+def bs_sched_counts(s: Scheduler) -> dict:
+    return s.counts()
+
+
+def bs_sched_last_error() -> str:
+    return lib.bs_sched_last_error().decode()

@@ -15,6 +15,7 @@ import test_oracle_attention as TA
 import test_oracle_compact_step as TC
 import test_oracle_decode as TD
 import test_oracle_geometry as TG
+import test_schedule as TS
 
 
 def _mutant(modname: str, old: str, new: str):
@@ -42,6 +43,7 @@ DEC = "oracle.decode"
 GAT = "oracle.gather"
 GEO = "oracle.geometry"
 CMP = "oracle.compact"
+SCH = "oracle.schedule"
 
 MUTANTS = [
     # (module, anchor, replacement, exported name, pin tests that must catch it)
@@ -95,6 +97,15 @@ MUTANTS = [
     (CMP, "out_k[l, dr, h, dc:dc + ln] = sk[l, sr, h, sc:sc + ln]",
      "out_k[l, dr, h, dc:dc + ln] = sk[l, dr, h, sc:sc + ln]", "kv_scatter_compact",
      [(TC.test_stable_slot_plan_leaves_survivors_untouched,)]),
+    (SCH, "return self.p + (self.b + 1) * self.L", "return self.p + self.b * self.L", "schedule",
+     [(TS.test_eq1_cost_matches_bounding_box_definition,), (TS.test_fig1_example2_bounding_box_shrink_expands_the_batch,)]),
+    (SCH, "if c.p + self.L <= box and cost(self.active, c) <= self.budget:",
+     "if False and c.p + self.L <= box and cost(self.active, c) <= self.budget:", "schedule",
+     [(TS.test_admission_postconditions_and_completion, 2)]),
+    (SCH, "if r.b >= r.K or r.id in eos:", "if r.b >= r.K:", "schedule",
+     [(TS.test_eos_evicts_at_the_block_boundary,)]),
+    (SCH, "len(self.active) < self.fixed_batch", "len(self.active) <= self.fixed_batch", "schedule",
+     [(TS.test_fig1_example1_eviction_and_refill,)]),
 ]
 
 
@@ -105,5 +116,8 @@ def test_pins_catch_planted_mistake(monkeypatch, modname, old, new, name, pins):
     for pin in pins:
         assert not _fails(pin[0], *pin[1:]), f"{pin[0].__name__} fails on the real oracle"
     m = _mutant(modname, old, new)
-    monkeypatch.setattr(oracle, name, getattr(m, name))
+    if modname == SCH:                   # the scheduler pins use the module itself
+        monkeypatch.setattr(TS, "osch", m)
+    else:
+        monkeypatch.setattr(oracle, name, getattr(m, name))
     assert any(_fails(pin[0], *pin[1:]) for pin in pins), "no pin caught the planted mistake"

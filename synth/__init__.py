@@ -413,3 +413,64 @@ def gen_stage_row(w: Workload, layer: int, step: int, a: int, Wst: int):
     ks = _normal(rng(w.cfg, w.variant, S_STAGE, step, layer, a, 0), (w.Hkv, Wst, w.D), w.kv_sigma)
     vs = _normal(rng(w.cfg, w.variant, S_STAGE, step, layer, a, 1), (w.Hkv, Wst, w.D), w.kv_sigma)
     return _cast(w, ks), _cast(w, vs)
+
+
+# ---------------------------------------------------------------- closed-loop serving streams
+S_SERVE_LOGITS, S_SERVE_PROMPT, S_SERVE_STREAM = 20, 21, 22
+
+# Spike margins of the serving logits: sigmoid(m) of consecutive entries differ
+# by >= 0.018 and none lies within 0.019 of 0.9, so every selection decision of
+# the serving stream is far from the threshold and from ties.
+SERVE_MARGINS = np.array([0.2, 0.65, 1.1, 1.55, 2.0, 2.45, 2.9, 3.35], np.float64)
+
+
+def serve_stream(n: int, L: int, *, variant: int = 0, p_range=(4, 40), blocks=(1, 2, 3, 4)):
+    """Seeded request stream [(id, p, g)] with prompt lengths spread over
+    p_range and generation lengths of 1..4 blocks (some ending mid-block)."""
+    g_ = rng(900, variant, S_SERVE_STREAM)
+    out = []
+    for i in range(n):
+        p = int(g_.integers(p_range[0], p_range[1], endpoint=True))
+        k = int(g_.choice(blocks))
+        g = k * L - (int(g_.integers(0, L // 2)) if g_.random() < 0.3 else 0)
+        out.append((i, p, g))
+    return out
+
+
+def serve_prompt_row(rid: int, p: int, g: int, W: int, V: int, mask_id: int, variant: int = 0):
+    """Token and mask rows of an admitted request, right-aligned in a row of W
+    columns: prompt ids in [2, V), generation positions masked."""
+    g_ = rng(901, variant, S_SERVE_PROMPT, rid)
+    tok = np.zeros(W, np.int32)
+    msk = np.zeros(W, np.uint8)
+    off = W - (p + g)
+    tok[off:off + p] = g_.integers(2, V, size=p, dtype=np.int32)
+    tok[off + p:] = mask_id
+    msk[off + p:] = 1
+    return tok, msk
+
+
+def serve_logits(ids, descs, step: int, V: int, L: int, eos_id: int, eos_block: dict,
+                 variant: int = 0) -> np.ndarray:
+    """Logits [n][L][V] fp32 for one denoising step of the active requests
+    (descriptor k = block index). Every position gets N(0,1) logits plus a
+    spiked id (LSE of the others + a margin from SERVE_MARGINS, a permutation
+    per request, block and step, so no two positions of a block tie). A request
+    listed in eos_block spikes eos_id at position 0 of that block."""
+    out = np.zeros((len(ids), L, V), np.float32)
+    for i, (rid, d) in enumerate(zip(ids, descs)):
+        b = int(d["k"])
+        g_ = rng(902, variant, S_SERVE_LOGITS, int(rid), b, step)
+        x = g_.standard_normal((L, V)).astype(np.float32)
+        perm = g_.permutation(len(SERVE_MARGINS))
+        sid = g_.integers(2, V, size=L)
+        for j in range(L):
+            if eos_block.get(int(rid), -1) == b and j == 0:
+                sid[j] = eos_id
+            row = x[j].astype(np.float64)
+            row[sid[j]] = -np.inf
+            mx = row.max()
+            lse = mx + math.log(np.exp(row - mx).sum())
+            x[j, sid[j]] = np.float32(lse + SERVE_MARGINS[perm[j % len(perm)]])
+        out[i] = x
+    return out

@@ -180,6 +180,92 @@ def traffic_summary(args, workload):
     print("\n".join(lines))
 
 
+class DeviceProvider:
+    """Model stand-in for the serving bench: inputs of the right shapes and
+    distributions made once on the device (queries, fresh block KV, spiked
+    logits whose max probability spreads around the threshold) and reused by
+    every step; prefilled KV drawn per admission. Seeded torch generator."""
+
+    def __init__(self, cfg, seed=11):
+        import torch
+        self.torch, self.cfg = torch, cfg
+        g = self.gen = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        R, L, td = cfg.rows, cfg.L, torch.bfloat16
+        s = 1.0 / np.sqrt(cfg.D)
+        self.layers = [(torch.randn((R, L, cfg.Hq, cfg.D), generator=g, device="cuda").to(td),
+                        (torch.randn((R, L, cfg.Hkv, cfg.D), generator=g, device="cuda") * s).to(td),
+                        (torch.randn((R, L, cfg.Hkv, cfg.D), generator=g, device="cuda") * s).to(td))
+                       for _ in range(cfg.layers)]
+        x = torch.randn((R * L, cfg.V), generator=g, device="cuda")
+        sid = torch.randint(2, cfg.V, (R * L,), generator=g, device="cuda")
+        m = torch.rand((R * L,), generator=g, device="cuda") * 8.0
+        x.scatter_(1, sid[:, None], (torch.logsumexp(x, dim=1) + m)[:, None])
+        self.logits = x.view(R, L, cfg.V).to(td)
+        self.prompt_rng = np.random.default_rng(seed)
+
+    def prefill(self, ids, p, g, W):
+        torch, cfg = self.torch, self.cfg
+        n, ws = len(ids), int((p + g).max())
+        s = 1.0 / np.sqrt(cfg.D)
+        sk = (torch.randn((cfg.layers, n, cfg.Hkv, ws, cfg.D), generator=self.gen, device="cuda") * s).to(torch.bfloat16)
+        sv = (torch.randn((cfg.layers, n, cfg.Hkv, ws, cfg.D), generator=self.gen, device="cuda") * s).to(torch.bfloat16)
+        tok = np.zeros((n, W), np.int32)
+        msk = np.zeros((n, W), np.uint8)
+        for a in range(n):
+            off = W - int(p[a] + g[a])
+            tok[a, off:off + int(p[a])] = self.prompt_rng.integers(2, cfg.V, int(p[a]))
+            msk[a, off + int(p[a]):] = 1
+        return sk, sv, tok, msk
+
+    def step(self, ids, descs, cycle, step):
+        n = len(ids)
+        return [(q[:n], kn[:n], vn[:n]) for q, kn, vn in self.layers], self.logits[:n]
+
+
+def serve_bench(args):
+    """Closed-loop serving of a stream shaped like one row of the benchmark
+    statistics table; prints one JSON line."""
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+    from paper_2607_08930_amd import serve
+
+    torch.cuda.set_device(0)
+    stream = synth.table_stream(args.serve, args.serve_requests)
+    pa, pm, limit, ga, gm = synth.TABLE_STREAMS[args.serve]
+    W = max(p + g for _, p, g in stream)
+    B = args.batch
+    budget = args.budget if args.budget else B * (pa + limit)
+    policy = bs.SCHED_FIXED if args.policy == "fixed" else bs.SCHED_BUDGET
+    rows = B if policy == bs.SCHED_FIXED else args.rows
+    cfg = serve.ServeConfig(L=32, layers=args.layers, Hq=32, Hkv=32, D=128, V=126464, dtype="bf16", rows=rows,
+                            width=W, policy=policy, budget=budget, fixed_batch=B, tau=0.9, q_min=1, eos_id=-1)
+    print(f"[bench] serving {args.serve} x{len(stream)} ({args.policy}, B={B}, budget={budget}, rows={rows}, W={W})",
+          file=sys.stderr, flush=True)
+    prov = DeviceProvider(cfg)
+    with bs.Context(0) as ctx:
+        serve.Server(ctx, cfg, prov).run(stream[:8])            # warm-up on a few requests
+        torch.cuda.synchronize()
+        srv = serve.Server(ctx, cfg, prov)
+        t0 = time.perf_counter()
+        res = srv.run(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    gen = sum(g for _, _, g in stream)
+    R = sum(res.active_counts) / (res.cycles * B)
+    print(json.dumps({
+        "metric": "closed-loop generated tokens/s", "value": round(gen / wall, 1), "unit": "tokens/s",
+        "n_gpus": 1, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"serve-{args.serve}-llada8b-layer", "requests": len(stream), "policy": args.policy,
+                   "baseline_batch": B, "budget_tokens": budget, "rows": rows, "W": W, "layers": args.layers,
+                   "stream": "prompt/generated lengths shaped like the benchmark statistics table row"},
+        "wall_s": round(wall, 3), "block_cycles": res.cycles, "denoising_steps": res.steps,
+        "generated_tokens": gen, "steps_per_cycle": round(res.steps / res.cycles, 2),
+        "mean_active": round(sum(res.active_counts) / res.cycles, 2), "R_eq2": round(R, 3),
+        "ms_per_step": round(wall * 1e3 / res.steps, 4)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,7 +278,22 @@ def main():
                     help="run one 256 MiB device copy first (the reference kernel for FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs into profiles/traffic_<workload>.md (no GPU needed)")
+    ap.add_argument("--serve", choices=["humaneval-256", "gsm8k-256", "mbpp-512", "truthfulqa-512"],
+                    help="closed-loop serving of a table-shaped request stream instead of the step bench")
+    ap.add_argument("--serve-requests", type=int, default=256)
+    ap.add_argument("--policy", choices=["budget", "fixed"], default="budget")
+    ap.add_argument("--batch", type=int, default=16, help="fixed cap, and B of Eq. 2")
+    ap.add_argument("--budget", type=int, default=0, help="Eq. 1 budget in tokens (default B * (avg prompt + limit))")
+    ap.add_argument("--rows", type=int, default=128, help="rows of the dense box under the budget policy")
+    ap.add_argument("--layers", type=int, default=1)
     args = ap.parse_args()
+    if args.serve:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        serve_bench(args)
+        return
     if args.traffic_summary:
         import synth
         traffic_summary(args, synth.workload(args.config).name)

@@ -474,3 +474,34 @@ def serve_logits(ids, descs, step: int, V: int, L: int, eos_id: int, eos_block: 
             x[j, sid[j]] = np.float32(lse + SERVE_MARGINS[perm[j % len(perm)]])
         out[i] = x
     return out
+
+
+# Prompt and generated lengths shaped like the benchmark statistics table
+# (LLaDA tokenizer): (prompt avg, prompt max, generation limit, actual avg,
+# actual max). Only these summary numbers are used; no benchmark item is.
+TABLE_STREAMS = {
+    "humaneval-256": (157, 423, 256, 231, 255),
+    "gsm8k-256": (1020, 1632, 256, 231, 260),
+    "mbpp-512": (750, 4332, 512, 284, 512),
+    "truthfulqa-512": (198, 245, 512, 33, 510),
+}
+
+
+def _shaped(g: np.random.Generator, n: int, avg: float, mx: int, lo: int, sigma: float) -> np.ndarray:
+    """n integers in [lo, mx] with mean close to avg: a lognormal spread around
+    avg, clipped, then rescaled once so the clipped mean matches."""
+    x = np.exp(g.normal(0.0, sigma, n) - sigma * sigma / 2.0) * avg
+    x = np.clip(x, lo, mx)
+    x = np.clip(x * (avg / x.mean()), lo, mx)
+    return np.rint(x).astype(np.int64)
+
+
+def table_stream(name: str, n: int, variant: int = 0):
+    """[(id, p, g)]: g is the generated length (the request ends there, as
+    CheckEOS would end it), at most the generation limit."""
+    pa, pm, limit, ga, gm = TABLE_STREAMS[name]
+    g_ = rng(903, variant, S_SERVE_STREAM, sum(map(ord, name)))
+    p = _shaped(g_, n, pa, pm, 8, 0.6)
+    sig = 1.2 if ga < 0.3 * limit else 0.25
+    gen = _shaped(g_, n, ga, min(gm, limit), 1, sig)
+    return [(i, int(p[i]), int(gen[i])) for i in range(n)]

@@ -182,35 +182,27 @@ __device__ inline void dma16_sv(uint32_t lds, uint64_t base, uint32_t off) {
                : "memory");
 }
 
-// Wait until at most N (compile time) / n (run time, wave-uniform) of this
-// wave's vector-memory operations are outstanding. gfx9 encoding:
-// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]; counts above 63
-// wait for everything.
+// Wait until at most N (compile time) of this wave's vector-memory operations
+// are outstanding. gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
+// vmcnt_hi[15:14]; counts above 63 wait for everything.
 template <int N>
 __device__ inline void wait_vm_c() {
   constexpr int n = N > 63 ? 0 : N;
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-__device__ inline void wait_vm(int n) {
-#define BS_VM(N) case N: wait_vm_c<N>(); break;
-  switch (n) {
-    BS_VM(0) BS_VM(1) BS_VM(2) BS_VM(3) BS_VM(4) BS_VM(5) BS_VM(6) BS_VM(7) BS_VM(8) BS_VM(9)
-     BS_VM(10) BS_VM(11) BS_VM(12) BS_VM(13) BS_VM(14) BS_VM(15) BS_VM(16) BS_VM(17) BS_VM(18) BS_VM(19)
-     BS_VM(20) BS_VM(21) BS_VM(22) BS_VM(23) BS_VM(24) BS_VM(25) BS_VM(26) BS_VM(27) BS_VM(28) BS_VM(29)
-     BS_VM(30) BS_VM(31) BS_VM(32) BS_VM(33) BS_VM(34) BS_VM(35) BS_VM(36) BS_VM(37) BS_VM(38) BS_VM(39)
-     BS_VM(40) BS_VM(41) BS_VM(42) BS_VM(43) BS_VM(44) BS_VM(45) BS_VM(46) BS_VM(47) BS_VM(48) BS_VM(49)
-     BS_VM(50) BS_VM(51) BS_VM(52) BS_VM(53) BS_VM(54) BS_VM(55) BS_VM(56) BS_VM(57) BS_VM(58) BS_VM(59)
-     BS_VM(60) BS_VM(61) BS_VM(62) BS_VM(63)
-    default: wait_vm_c<0>(); break;
-  }
-#undef BS_VM
 }
 
 // One (request, KV head) item processed by GW waves that share its K/V tiles:
 // wave wg of the group serves query head c * G + wg / RB and rows
 // 32 * (wg % RB) .. + 32 of the block. SHARED = false is the single-wave case
 // (GW = 1): the wave owns its ring, so no barrier is needed anywhere.
-template <int D, int KT, int NS, bool SHARED, int MAXBLK>
+//
+// The DMA of a stage (2 * BPT blocks of 1 KiB) is issued by the NI waves
+// I0 .. I0 + NI - 1 only, PB = 2 * BPT / NI blocks each, so every count and
+// offset of the issue sequence is a compile-time constant plus one per-wave
+// base: no per-block branch, and the waits are compile-time vmcnt values.
+// The other waves see a stage through the barrier that follows the issuers'
+// waits.
+template <int D, int KT, int NS, bool SHARED, int NI, int I0>
 __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t* ring, int GW, int wg,
                                  int lane) {
   constexpr int NKK = D / 16;
@@ -220,6 +212,9 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   constexpr int BPT = KT / RPB;                   // blocks per K (or V) tile
   constexpr int TILE = KT * D;                    // elements of one K (or V) tile
   constexpr int STAGE = 2 * TILE;                 // K tile then V tile
+  constexpr int RPI = BPT / NI;                   // blocks per tile and issuing wave
+  constexpr int PB = 2 * RPI;                     // blocks per stage and issuing wave
+  static_assert(BPT % NI == 0, "issuing waves must split a tile evenly");
   const int g = lane >> 5, n = lane & 31;
   const int c = it.kvh;
   const int h = c * a.G + wg / a.RB;
@@ -233,54 +228,64 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   const uint16_t* knb = static_cast<const uint16_t*>(a.k_new) + ((int64_t)it.req * a.L * a.Hkv + c) * D;
   const uint16_t* vnb = static_cast<const uint16_t*>(a.v_new) + ((int64_t)it.req * a.L * a.Hkv + c) * D;
 
-  // DMA work of this wave per stage: blocks wg, wg + GW, ... of the 2 * BPT.
-  // Block bi covers rows [rb * RPB, rb * RPB + RPB) of tensor bi / BPT; lane l
-  // fills slot l % NCH of row rb * RPB + l / NCH with global chunk slot ^ swz(row).
-  const int nblk = (2 * BPT - wg + GW - 1) / GW;
-  const int drow = lane / NCH, dslot = lane % NCH;
-  uint32_t doff[MAXBLK];                          // byte offset of this lane's chunk within a tile
-#pragma unroll
-  for (int k = 0; k < MAXBLK; ++k) {
-    const int bi = min(wg + k * GW, 2 * BPT - 1);
-    const int row = (bi % BPT) * RPB + drow;
-    doff[k] = (uint32_t)(row * D + ((dslot ^ swz<NCH>(row)) * 8)) * 2u;
-  }
-  const uint32_t ring_lds = lds_addr(ring);
+  // Block k of issuing wave u = wg - I0 is block (k % RPI) * NI + u of tensor
+  // k / RPI (K, then V): it covers tile rows [rb * RPB, rb * RPB + RPB), and
+  // lane l fills slot l % NCH of row rb * RPB + l / NCH with global chunk
+  // slot ^ swz(row).
+  const bool issuer = (unsigned)(wg - I0) < (unsigned)NI;
+  const int u = issuer ? wg - I0 : 0;
+  const int urow = u * RPB + lane / NCH, dslot = lane % NCH;
+  const uint32_t ring_lds = lds_addr(ring) + (uint32_t)(u * RPB * D * 2);
+  auto row_of = [&](int r) { return r * NI * RPB + urow; };
+  auto chunk_of = [&](int row) { return dslot ^ swz<NCH>(row); };
   auto issue = [&](int stage, int tb) {
     const uint32_t sbase = __builtin_amdgcn_readfirstlane(ring_lds + (uint32_t)(stage * STAGE * 2));
     if (tb + KT <= len && (tb + KT <= bs || tb >= be)) {
       // whole tile inside the cached part of the row: uniform base + lane offset
       const uint64_t kb = uniform64(kcb + (int64_t)tb * D), vb = uniform64(vcb + (int64_t)tb * D);
 #pragma unroll
-      for (int k = 0; k < MAXBLK; ++k) {
-        if (k < nblk) {
-          const int bi = wg + k * GW;
-          const int tensor = bi / BPT, rb = bi - tensor * BPT;
-          dma16_sv(sbase + (uint32_t)((tensor * TILE + rb * RPB * D) * 2), tensor ? vb : kb, doff[k]);
-        }
+      for (int k = 0; k < PB; ++k) {
+        const int tensor = k / RPI, r = k % RPI;
+        const int row = row_of(r);
+        dma16_sv(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), tensor ? vb : kb,
+                 (uint32_t)(row * D + chunk_of(row) * 8) * 2u);
       }
     } else {
       // tile holds fresh block rows or runs past the row end: per-lane sources
-      for (int k = 0; k < nblk; ++k) {
-        const int bi = wg + k * GW;
-        const int tensor = bi / BPT, rb = bi - tensor * BPT;
-        const int row = rb * RPB + drow;
+#pragma unroll
+      for (int k = 0; k < PB; ++k) {
+        const int tensor = k / RPI, r = k % RPI;
+        const int row = row_of(r);
         const int t = min(tb + row, len - 1);        // rows past the end repeat a valid key (masked later)
         const bool fresh = (t >= bs) & (t < be);
         const uint16_t* src = tensor ? (fresh ? vnb + (int64_t)(t - bs) * fstride : vcb + (int64_t)t * D)
                                      : (fresh ? knb + (int64_t)(t - bs) * fstride : kcb + (int64_t)t * D);
-        const int chunk = dslot ^ swz<NCH>(row);
-        dma16(sbase + (uint32_t)((tensor * TILE + rb * RPB * D) * 2), src + chunk * 8);
+        dma16(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), src + chunk_of(row) * 8);
       }
     }
+  };
+  // issuing waves: wait until at most x (< NS) stages of this wave's DMA are
+  // in flight (a count above the 6-bit vmcnt field waits for everything)
+  auto wait_stages = [&](int x) {
+    static_assert(NS <= 4, "wait counts are encoded up to three stages");
+    if (x <= 0)
+      wait_vm_c<0>();
+    else if (x == 1)
+      wait_vm_c<PB>();
+    else if (x == 2)
+      wait_vm_c<2 * PB>();
+    else
+      wait_vm_c<3 * PB>();
   };
 
   const int ntiles = (len + KT - 1) / KT;
   // prologue: stages 0 .. NS-2 (issued before anything else so the first
   // tiles are in flight while the queries load)
+  if (issuer) {
 #pragma unroll
-  for (int st = 0; st < NS - 1; ++st)
-    if (st < ntiles) issue(st, st * KT);
+    for (int st = 0; st < NS - 1; ++st)
+      if (st < ntiles) issue(st, st * KT);
+  }
 
   // queries of this lane's column as MFMA B operands: feature d = 16 kk + 8 g + e
   bf16x8_t qb[NKK];
@@ -363,7 +368,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
     };
 
     // tile 0 resident (the later prologue stages may still be in flight)
-    wait_vm(nblk * min(ntiles - 1, NS - 2));
+    if (issuer) wait_stages(min(ntiles - 1, NS - 2));
     __syncthreads();
     f32x16_t sa, sb;
     scores(ring, sa, sb);
@@ -371,10 +376,10 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       if (tile + 1 < ntiles) {
         // tile + 1 landed (stages up to tile + NS - 2 were issued); after the
         // barrier every wave is done with tile - 1, whose slot is refilled
-        wait_vm(nblk * max(0, min(ntiles - 1, tile + NS - 2) - tile - 1));
+        if (issuer) wait_stages(min(ntiles - 1, tile + NS - 2) - tile - 1);
         __syncthreads();
         const int nxt = tile + NS - 1;
-        if (nxt < ntiles) issue(nxt % NS, nxt * KT);
+        if (issuer && nxt < ntiles) issue(nxt % NS, nxt * KT);
       }
       const int tb = tile * KT;
       if (tb + KT > len) {                         // ragged last tile only
@@ -415,10 +420,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       if (nxt < ntiles) issue(nxt % NS, nxt * KT);
       // this tile's stage has landed once only the later stages' DMAs remain
       // (a single wave issues all 2 * BPT blocks of a stage)
-      if (tile + NS <= ntiles)
-        wait_vm_c<2 * BPT * (NS - 1)>();
-      else
-        wait_vm(nblk * (ntiles - tile - 1));
+      wait_stages(min(NS - 1, ntiles - tile - 1));
       const uint16_t* kt = ring + (tile % NS) * STAGE;
       const uint16_t* vtl = kt + TILE;
       const int tb = tile * KT;
@@ -543,18 +545,17 @@ __global__ __launch_bounds__(64 * NW, 1) void k_attn_bf16_wave(AttnArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int idx = blockIdx.x * NW + w;
   if (idx >= a.n_items) return;
-  attn_item<D, 32, NS, false, 2 * (32 * D / 512)>(a, a.items[idx], lds + w * NS * STAGE, 1, 0, threadIdx.x & 63);
+  attn_item<D, 32, NS, false, 1, 0>(a, a.items[idx], lds + w * NS * STAGE, 1, 0, threadIdx.x & 63);
 }
 
-// GW = G * ceil(L / 32) >= 2 waves share each item's 64-key tiles.
-template <int D, int NS, int GWMIN>
+// GW = G * ceil(L / 32) >= 2 waves share each item's 64-key tiles; the first
+// NI <= GW of them issue its DMA.
+template <int D, int NS, int NI>
 __global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
   constexpr int STAGE = 2 * 64 * D;
-  constexpr int BLK = 2 * (64 * D / 512);         // DMA blocks per stage
   __shared__ __align__(1024) uint16_t lds[NS * STAGE];
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  attn_item<D, 64, NS, true, (BLK + GWMIN - 1) / GWMIN>(a, a.items[blockIdx.x], lds, blockDim.x >> 6, w,
-                                                         threadIdx.x & 63);
+  attn_item<D, 64, NS, true, NI, 0>(a, a.items[blockIdx.x], lds, blockDim.x >> 6, w, threadIdx.x & 63);
 }
 
 template <int D>
@@ -562,10 +563,10 @@ hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   if (GW == 1) {
     constexpr int NS = 2, NW = kMhaWaves;
     hipLaunchKernelGGL((k_attn_bf16_wave<D, NS, NW>), dim3((a.n_items + NW - 1) / NW), dim3(64 * NW), 0, s, a);
-  } else if (GW <= 4) {
+  } else if (GW < 4) {
     hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 2>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 5>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
+    hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 4>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -156,7 +156,7 @@ int bs_scatter_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int 
  * cells [off_i + s_i + j] of head c (no other cache cell is written); with 0
  * the caches are only read.
  * Supported: Hq % Hkv == 0; BS_F32 with D % 4 == 0, D <= 256; BS_BF16 with
- * D in {64, 128}, L <= 64 and (Hq / Hkv) * ceil(L / 32) <= 8. All pointers
+ * D in {64, 128}, L <= 64 and Hq / Hkv <= 8. All pointers
  * 16-byte aligned. Cache cells outside each request's logical row and the
  * stale block slot are never read (they may hold NaN).
  * ws: device workspace of at least bs_attention_workspace_bytes(...) bytes

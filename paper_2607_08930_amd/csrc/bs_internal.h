@@ -42,7 +42,7 @@ struct AttnItem {
   int32_t B;     // block length
   int32_t row;   // dense row of the cache
   int32_t off;   // column of logical position 0
-  int32_t pad;
+  int32_t rb;    // first 32-row block of the block served by this workgroup
 };
 
 struct AttnArgs {
@@ -50,6 +50,7 @@ struct AttnArgs {
   const AttnItem* items;
   int n_items;
   int L, Hq, Hkv, D, G, RB;  // RB: 32-row blocks per head = ceil(L / 32)
+  int RBW;                   // row blocks per workgroup: RB, or 1 when G * RB > 8 waves
   int R, W;
   float scale_log2e;         // softmax scale * log2(e)
   float scale;               // softmax scale

@@ -230,8 +230,9 @@ int check_attention(bs_ctx* c, int n, int L, int Hq, int Hkv, int D, bs_dtype dt
     return fail(c, BS_ERR_UNSUPPORTED, "fp32 path needs D %% 4 == 0 and D <= 256 (D=%d)", D);
   if (dt == BS_BF16) {
     if (D != 64 && D != 128) return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs D in {64, 128} (D=%d)", D);
-    if (L > 64 || G * RB > 8)
-      return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs L <= 64 and (Hq/Hkv)*ceil(L/32) <= 8 (got %d)", G * RB);
+    if (L > 64 || G > 8)
+      return fail(c, BS_ERR_UNSUPPORTED, "bf16 path needs L <= 64 and Hq/Hkv <= 8 (L=%d, Hq/Hkv=%d)", L, G);
+    (void)RB;
   }
   return BS_OK;
 }
@@ -259,9 +260,14 @@ void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, i
   if (dt == BS_BF16) {
     std::vector<AttnItem> items;
     items.reserve((size_t)n * Hkv);
+    // one workgroup per (request, KV head), or per (request, KV head, 32-row
+    // block) when the query group times the row blocks exceeds 8 waves
+    const int RB = (L + 31) / 32, split = (Hq / Hkv) * RB > 8 ? RB : 1;
     for (int i = 0; i < n; ++i) {
       const Geo gq = geo_of(reqs[i], L);
-      for (int h = 0; h < Hkv; ++h) items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, 0});
+      for (int h = 0; h < Hkv; ++h)
+        for (int rb = 0; rb < split; ++rb)
+          items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, rb});
     }
     std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
     const size_t N = items.size();
@@ -284,6 +290,7 @@ AttnArgs attention_args(const Slot* sl, int L, int Hq, int Hkv, int D, int R, in
   a.items = reinterpret_cast<const AttnItem*>(base + sl->meta[1]);
   a.n_items = sl->meta[2];
   a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = Hq / Hkv; a.RB = (L + 31) / 32; a.R = R; a.W = W;
+  a.RBW = a.G * a.RB > 8 ? 1 : a.RB;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
   a.scale_log2e = a.scale * 1.4426950408889634f;
   a.write_back = write_back ? 1 : 0;

@@ -192,8 +192,9 @@ __device__ inline void wait_vm_c() {
 }
 
 // One (request, KV head) item processed by GW waves that share its K/V tiles:
-// wave wg of the group serves query head c * G + wg / RB and rows
-// 32 * (wg % RB) .. + 32 of the block. SHARED = false is the single-wave case
+// wave wg of the group serves query head c * G + wg / RBW and rows
+// 32 * (rb + wg % RBW) .. + 32 of the block (RBW row blocks per workgroup,
+// starting at the item's rb). SHARED = false is the single-wave case
 // (GW = 1): the wave owns its ring, so no barrier is needed anywhere.
 //
 // The DMA of a stage (2 * BPT blocks of 1 KiB) is issued by the NI waves
@@ -217,8 +218,8 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   static_assert(BPT % NI == 0, "issuing waves must split a tile evenly");
   const int g = lane >> 5, n = lane & 31;
   const int c = it.kvh;
-  const int h = c * a.G + wg / a.RB;
-  const int j = (wg % a.RB) * 32 + n;
+  const int h = c * a.G + wg / a.RBW;
+  const int j = (it.rb + wg % a.RBW) * 32 + n;
   const int bs = it.s, be = it.s + it.B, len = it.len;
 
   const int64_t cache_off = (((int64_t)it.row * a.Hkv + c) * a.W + it.off) * D;
@@ -486,8 +487,9 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   }
   const float lt = lsum + __shfl_xor(lsum, 32, 64);
   // in-place KV update: the group's waves store the fresh block rows of this
-  // KV head into the cache slot [off + s, off + s + B)
-  if (a.write_back) {
+  // KV head into the cache slot [off + s, off + s + B) (one workgroup per
+  // KV head does it when the row blocks are split over several)
+  if (a.write_back && it.rb == 0) {
     constexpr int MAXWB = 32 * D / 8 / 64;          // per wave, for a 32-row block
     uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
     uint16_t* vcw = static_cast<uint16_t*>(a.v_cache) + cache_off;
@@ -581,7 +583,7 @@ hipError_t launch_attn_f32(const AttnArgs& a, int n_req, hipStream_t s) {
 }
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t s) {
-  const int GW = a.G * a.RB;
+  const int GW = a.G * a.RBW;
   if (a.D == 128) return launch_bf16_d<128>(a, GW, s);
   if (a.D == 64) return launch_bf16_d<64>(a, GW, s);
   return hipErrorInvalidValue;

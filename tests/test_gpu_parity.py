@@ -231,7 +231,8 @@ def test_attention_skewed_budget(ctx):
 
 def test_attention_edge_geometries(ctx):
     # partial last blocks, empty prompt, empty suffix, rows out of order, D=64,
-    # L=8 and L=64 (two row blocks per head), GQA and MHA
+    # L=8 and L=64 (two row blocks per head), GQA and MHA; 7 heads x 2 row
+    # blocks exceed one workgroup's 8 waves and are split by row block
     cases = [
         ("bf16 L8 partial", synth.custom(8, 4, 2, 128, 10, "bf16", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8],
                                           [1, 0, 1, 2, 0], W=40, rows=[2, 0, 4, 1, 3], kv_sigma=0.1)),
@@ -242,6 +243,10 @@ def test_attention_edge_geometries(ctx):
         ("bf16 G7 L32", synth.custom(32, 28, 4, 128, 10, "bf16", [1, 700], [40, 512], [1, 15], kv_sigma=0.1,
                                       q_sigma=4.0)),
         ("fp32 D128 G2", synth.custom(16, 4, 2, 128, 10, "f32", [3, 40], [20, 33], [1, 2])),
+        ("bf16 G7 L64 split", synth.custom(64, 28, 4, 128, 10, "bf16", [3, 300, 0], [64, 130, 40], [0, 1, 0],
+                                            rows=[2, 0, 1], kv_sigma=0.1, q_sigma=3.0)),
+        ("bf16 G8 L64 split", synth.custom(64, 16, 2, 64, 10, "bf16", [77, 5], [200, 64], [3, 0],
+                                            kv_sigma=0.1)),
     ]
     for label, w in cases:
         _att(ctx, w, label)
@@ -279,7 +284,7 @@ def test_attention_batch_invariance_and_determinism(ctx):
 
 def test_attention_rejects_unsupported(ctx):
     torch, bs, _ = lazy()
-    w = synth.custom(64, 28, 4, 128, 10, "bf16", [3], [64], [0])   # 7 heads x 2 row blocks > 8 waves
+    w = synth.custom(32, 36, 4, 128, 10, "bf16", [3], [64], [0])   # 9 query heads per KV head > 8 waves
     with pytest.raises(bs.BlockServeError, match="UNSUPPORTED"):
         run_attention(ctx, w)
     w = synth.custom(32, 3, 2, 128, 10, "bf16", [3], [64], [0])    # Hq % Hkv != 0

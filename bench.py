@@ -286,6 +286,10 @@ def main():
     ap.add_argument("--budget", type=int, default=0, help="Eq. 1 budget in tokens (default B * (avg prompt + limit))")
     ap.add_argument("--rows", type=int, default=128, help="rows of the dense box under the budget policy")
     ap.add_argument("--layers", type=int, default=1)
+    ap.add_argument("--block-length", type=int, default=None,
+                    help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
+    ap.add_argument("--prefix-only", action="store_true",
+                    help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
     if args.serve:
         if args.gpus != 1:
@@ -296,7 +300,8 @@ def main():
         return
     if args.traffic_summary:
         import synth
-        traffic_summary(args, synth.workload(args.config).name)
+        name = synth.workload(args.config, block_length=args.block_length).name
+        traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
@@ -310,7 +315,10 @@ def main():
 
     assert torch.cuda.is_available()
     torch.cuda.set_device(0)
-    w = synth.workload(args.config)
+    w = synth.workload(args.config, block_length=args.block_length)
+    if args.prefix_only:
+        w.reqs = bstep.prefix_only(w.reqs, w.L)
+        w.name += "-prefix-only"
     print(f"[bench] building inputs for {w.name}", file=sys.stderr, flush=True)
     st, host = build_state(w)
     ab = algorithmic_bytes(w)

@@ -155,6 +155,9 @@ int bs_scatter_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int 
  * write_back != 0 additionally stores k_new/v_new rows j < B_i into the cache
  * cells [off_i + s_i + j] of head c (no other cache cell is written); with 0
  * the caches are only read.
+ * Prefix-cache layout (keys = prompt, decoded blocks and the active block,
+ * without the masked suffix): pass g_i' = min(g_i, (k_i + 1) L) with the same
+ * off_i; the cells past the active block are then never read.
  * Supported: Hq % Hkv == 0; BS_F32 with D % 4 == 0, D <= 256; BS_BF16 with
  * D in {64, 128}, L <= 64 and Hq / Hkv <= 8. All pointers
  * 16-byte aligned. Cache cells outside each request's logical row and the

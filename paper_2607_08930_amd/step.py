@@ -148,3 +148,15 @@ def compact(ctx: Context, segs: np.ndarray, n_layers: int, Hkv: int, D: int, dty
                           layer_stride(stg_k) if stg_k is not None else 0,
                           stg_k.shape[1] if stg_k is not None else 1, stg_k.shape[3] if stg_k is not None else 1,
                           dst_k, dst_v, layer_stride(dst_k), dst_k.shape[1], dst_k.shape[3], stream=stream)
+
+
+def prefix_only(reqs: np.ndarray, L: int) -> np.ndarray:
+    """Descriptors for the prefix-cache layout (no masked suffix in the keys):
+    each request attends over its prompt, its decoded blocks and its active
+    block only, i.e. the Eq. 1 row width p + (k + 1) L (capped at p + g for a
+    partial last block). The dense box keeps its layout: g is cut to
+    min(g, (k + 1) L) and off is unchanged, so the same cells hold the same
+    positions and the kernels never read the cells past the active block."""
+    out = np.array(reqs, copy=True)
+    out["g"] = np.minimum(out["g"], (out["k"].astype(np.int64) + 1) * L).astype(out["g"].dtype)
+    return out

@@ -121,10 +121,15 @@ def make_reqs(p, g, k, *, W=None, rows=None) -> tuple[np.ndarray, int, int]:
     return reqs, R, int(W)
 
 
-def workload(cfg: int, variant: int = 0, **over) -> Workload:
+def workload(cfg: int, variant: int = 0, block_length: int | None = None, **over) -> Workload:
     """Build one of the five step workloads (1: tiny fp32, 2: LLaDA-8B-shaped,
     3: Dream-7B-shaped, 4: token-budgeted skewed Dream batch, 5: LLaDA-8B-shaped
-    32-layer churn). ``variant`` re-seeds every tensor; ``over`` overrides fields."""
+    32-layer churn). ``variant`` re-seeds every tensor; ``over`` overrides fields.
+
+    ``block_length`` (workloads 2-5, a divisor or multiple of 32 up to 64)
+    re-blocks the same requests at another L: block index k becomes
+    floor(32 k / L), so each request's active block starts at the same
+    position or the nearest block boundary below it."""
     r = rng(cfg, variant, S_DESC)
     if cfg == 1:
         reqs, R, W = make_reqs([5, 12, 7, 20], [16, 24, 8, 32], [1, 0, 0, 3])
@@ -174,6 +179,13 @@ def workload(cfg: int, variant: int = 0, **over) -> Workload:
     else:
         raise ValueError(f"unknown workload {cfg}")
     w.variant = variant
+    if block_length is not None and block_length != w.L:
+        if cfg == 1 or block_length not in (8, 16, 64):
+            raise ValueError(f"block_length {block_length} not offered for workload {cfg}")
+        w.reqs = w.reqs.copy()
+        w.reqs["k"] = (w.reqs["k"] * w.L) // block_length
+        w.name = w.name.replace(f"-L{w.L}", f"-L{block_length}")
+        w.L = block_length
     for kk, vv in over.items():
         setattr(w, kk, vv)
     return w

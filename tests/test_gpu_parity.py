@@ -150,6 +150,18 @@ def test_decode_fixed_quota_and_eos(ctx):
     got, ref, _ = _decode_case(ctx, w, "eos", eos_id=0)
 
 
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_decode_fixed_quota_full_size(ctx, cfg):
+    # the fixed-quota schedule (threshold disabled): every request unmasks
+    # exactly min(|M|, 2) positions, its two most confident (normal logits
+    # keep the confidence ranks apart; the spiked ones crowd them near 1)
+    w = synth.workload(cfg, logits="normal", logit_sigma=4.0)
+    _, _, blk = synth.gen_state(w)
+    got, ref, nex = _decode_case(ctx, w, f"cfg{cfg} quota 2", tau=1.5, q_min=2)
+    assert (got["n_unmasked"] == np.minimum(blk.sum(axis=1), 2)).all()
+    assert nex <= w.n // 4
+
+
 def test_decode_tiny_vocab_tail(ctx):
     # V not a multiple of the vector width exercises the element-wise tail
     w = synth.custom(8, 2, 2, 16, 37, "f32", [3, 7], [16, 12], [1, 1], logits="normal", logit_sigma=2.0)
@@ -259,6 +271,19 @@ def test_attention_poisoned_padding_and_stale_slot(ctx):
         b, _, _, _ = run_attention(ctx, w, poison=True)
         say(f"[attention poison cfg{cfg}]")
         assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_attention_prefix_only_layout(ctx, cfg):
+    # prefix-cache layout: keys end at the active block; the suffix cells are
+    # outside every logical row, so NaN there changes nothing
+    _, _, bstep = lazy()
+    w = synth.workload(cfg)
+    w.reqs = bstep.prefix_only(w.reqs, w.L)
+    _att(ctx, w, f"cfg{cfg} prefix-only")
+    a, _, _, _ = run_attention(ctx, w)
+    b, _, _, _ = run_attention(ctx, w, poison=True)
+    assert np.array_equal(a, b)
 
 
 def test_attention_no_write_back_leaves_cache(ctx):

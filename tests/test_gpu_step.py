@@ -97,6 +97,24 @@ def test_fused_step_matches_oracle(ctx, cfg):
     say(f"  exempt requests: {nex}")
 
 
+@pytest.mark.parametrize("cfg,L", [(2, 16), (2, 64), (3, 16), (3, 64)])
+def test_fused_step_block_length_sweep(ctx, cfg, L):
+    """The block-length ablation at kernel level: the same LLaDA- and
+    Dream-shaped requests re-blocked at L = 16 and 64 (at L = 64 the Dream
+    query groups are split into two row-block workgroups)."""
+    torch, bs, bstep = lazy()
+    w = synth.workload(cfg, block_length=L)
+    say(f"[fused step {w.name}] n={w.n} W={w.W}")
+    st, host = make_state(w)
+    bstep.run_step(ctx, st, w.reqs, want_conf=True)
+    torch.cuda.synchronize()
+    got = snapshot(st)
+    ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
+                                  tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+    nex = check_step(w, got, ref, host, w.name)
+    say(f"  exempt requests: {nex}")
+
+
 def test_churn_boundary_then_step_workload5(ctx):
     """Workload 5 shapes (MHA 32 x 128, L = 32, g = 128, V = 126464, W = 384):
     a seeded block-boundary churn plan rewrites the KV box in place (admitted

@@ -158,3 +158,30 @@ def test_gather_scatter_identities():
         assert np.array_equal(c2[i, :B], y[i, :B])
     changed = (box2 != box).any(axis=2).sum()
     assert changed <= sum(oracle.geometry(r, w.L).B for r in w.reqs)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+@pytest.mark.parametrize("L", [16, 64])
+def test_reblocked_workloads_are_valid_and_keep_block_starts(cfg, L):
+    # the block-length sweep re-blocks the same requests: every descriptor
+    # stays valid and the active block starts at the same position (L = 16)
+    # or at the block boundary at most 32 positions below it (L = 64)
+    w32 = synth.workload(cfg)
+    w = synth.workload(cfg, block_length=L)
+    assert w.L == L and f"-L{L}" in w.name
+    oracle.validate_reqs(w.reqs, w.L, w.R, w.W)
+    s32 = w32.reqs["p"] + 32 * w32.reqs["k"]
+    s = w.reqs["p"] + L * w.reqs["k"]
+    assert ((s32 - s) >= 0).all() and ((s32 - s) < max(L, 32)).all()
+    if L == 16:
+        assert (s == s32).all()
+    for r in w.reqs:
+        t = oracle.geometry(r, L)
+        assert 1 <= t.B <= L and t.s + t.B <= t.len
+
+
+def test_reblocking_rejects_unoffered_lengths():
+    with pytest.raises(ValueError):
+        synth.workload(2, block_length=48)
+    with pytest.raises(ValueError):
+        synth.workload(1, block_length=16)

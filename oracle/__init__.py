@@ -31,6 +31,8 @@ attention  block attention of the active block against the request's dual
 decode     confidence-aware parallel decoding with greedy (temperature 0)
            predictions and a per-step minimum quota (paragraph "Vectorized
            mixed-schedule execution"; "Implementation details").
+lm_head    the same decoding step with its logits produced by the output head
+           from the positions' hidden states (logits never stored).
 compact    KV scatter/compaction when requests are evicted and admitted at a
            block boundary (Algorithm 1; Eq. 1 discussion of the bounding box
            shrinking without explicit reclamation).
@@ -47,6 +49,7 @@ from .geometry import (geometry, validate_reqs, bbox_cost, position_ids, transfe
 from .gather import gather_active_blocks, scatter_active_blocks
 from .attention import dual_cache_block_attention, attention_rows
 from .decode import parallel_decode, row_stats
+from .lm_head import lm_head_logits, lm_head_decode
 from .compact import kv_scatter_compact
 from .step import mixed_state_step
 from . import schedule
@@ -56,5 +59,6 @@ __all__ = [
     "geometry", "validate_reqs", "bbox_cost", "position_ids", "transfer_schedule",
     "effective_compute_ratio", "widen", "gather_active_blocks", "scatter_active_blocks",
     "dual_cache_block_attention", "attention_rows", "parallel_decode", "row_stats",
+    "lm_head_logits", "lm_head_decode",
     "kv_scatter_compact", "mixed_state_step",
 ]

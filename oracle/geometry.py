@@ -11,7 +11,10 @@ import numpy as np
 
 
 def widen(x, dtype: str) -> np.ndarray:
-    """Exact fp64 value of an fp32 array, or of bf16 raw bit patterns (uint16)."""
+    """Exact fp64 value of an fp32 array, or of bf16 raw bit patterns (uint16);
+    an fp64 array ("f64": logits computed here, never stored) as it is."""
+    if dtype == "f64":
+        return np.asarray(x, dtype=np.float64)
     if dtype == "bf16":
         b = np.asarray(x, dtype=np.uint16)
         return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)

@@ -517,3 +517,41 @@ def table_stream(name: str, n: int, variant: int = 0):
     sig = 1.2 if ga < 0.3 * limit else 0.25
     gen = _shaped(g_, n, ga, min(gm, limit), 1, sig)
     return [(i, int(p[i]), int(gen[i])) for i in range(n)]
+
+
+# ---------------------------------------------------------------- output head
+S_LM_W, S_LM_H = 30, 31
+# model widths of the workloads' shapes (LLaDA-8B: 4096, Dream-7B: 3584)
+LM_HEAD_DIM = {1: 64, 2: 4096, 3: 3584, 4: 3584, 5: 4096}
+
+
+def gen_lm_weight(w: Workload, d: int, V: int | None = None) -> np.ndarray:
+    """Output-head matrix [V][d] as bf16 bits with N(0, 1/d) entries (the
+    logits of a unit-variance hidden state are then about N(0, 1)); rows are
+    drawn in chunks of 8192 from per-chunk streams."""
+    V = w.V if V is None else V
+    out = np.empty((V, d), np.uint16)
+    for c0 in range(0, V, 8192):
+        g = rng(w.cfg, w.variant, S_LM_W, c0 // 8192)
+        n = min(8192, V - c0)
+        out[c0:c0 + n] = f32_to_bf16_bits(g.standard_normal((n, d), dtype=np.float32) / np.float32(math.sqrt(d)))
+    return out
+
+
+def gen_lm_hidden(w: Workload, wv: np.ndarray) -> np.ndarray:
+    """Final hidden states [n][L][d] as bf16 bits: unit noise plus a component
+    along the head row of a random target token that lifts its logit to
+    ln(V) + 1/2 + m, m ~ U[-2, 6), about m above the log-sum-exp of the other
+    logits, so the max softmax probability spreads over roughly (0.1, 1)."""
+    V, d = wv.shape
+    out = np.zeros((w.n, w.L, d), np.uint16)
+    for i in range(w.n):
+        g = rng(w.cfg, w.variant, S_LM_H, i)
+        h = g.standard_normal((w.L, d), dtype=np.float32).astype(np.float64)
+        tgt = g.integers(1, V, size=w.L)
+        m = g.uniform(-2.0, 6.0, size=w.L)
+        for j in range(w.L):
+            wt = bf16_bits_to_f32(wv[tgt[j]]).astype(np.float64)
+            h[j] += (math.log(V) + 0.5 + m[j] - h[j] @ wt) / (wt @ wt) * wt
+        out[i] = f32_to_bf16_bits(h.astype(np.float32))
+    return out

@@ -15,6 +15,7 @@ import test_oracle_attention as TA
 import test_oracle_compact_step as TC
 import test_oracle_decode as TD
 import test_oracle_geometry as TG
+import test_oracle_lm_head as TL
 import test_schedule as TS
 
 
@@ -44,6 +45,7 @@ GAT = "oracle.gather"
 GEO = "oracle.geometry"
 CMP = "oracle.compact"
 SCH = "oracle.schedule"
+LMH = "oracle.lm_head"
 
 MUTANTS = [
     # (module, anchor, replacement, exported name, pin tests that must catch it)
@@ -106,6 +108,15 @@ MUTANTS = [
      [(TS.test_eos_evicts_at_the_block_boundary,)]),
     (SCH, "len(self.active) < self.fixed_batch", "len(self.active) <= self.fixed_batch", "schedule",
      [(TS.test_fig1_example1_eviction_and_refill,)]),
+    (LMH, "out[:, v0:v0 + chunk] = h @ widen(w_vocab[v0:v0 + chunk], dtype).T",
+     "out[:, v0:v0 + chunk] = h[:, 1:] @ widen(w_vocab[v0:v0 + chunk], dtype)[:, 1:].T", "lm_head_decode",
+     [(TL.test_matches_brute_force_products, 0, 3)]),
+    (LMH, "rows = {key: lg[a] for a, key in enumerate(keys)}",
+     "rows = {key: lg[min(a + 1, len(keys) - 1)] for a, key in enumerate(keys)}", "lm_head_decode",
+     [(TL.test_matches_brute_force_products, 1, 4096)]),
+    (LMH, "out[:, v0:v0 + chunk] = h @ widen(w_vocab[v0:v0 + chunk], dtype).T",
+     "out[:, v0:v0 + chunk] = h @ widen(w_vocab[v0:v0 + chunk][::-1], dtype).T", "lm_head_decode",
+     [(TL.test_identity_head_gives_softmax_of_the_hidden_state,)]),
 ]
 
 

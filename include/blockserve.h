@@ -206,6 +206,32 @@ int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V
                        void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * K3 with the output head fused in (paragraph "Vectorized mixed-schedule
+ * execution"; greedy parallel decoding, "Implementation details"): the same
+ * decoding step as bs_parallel_decode, with the logits of each masked
+ * position produced from its final hidden state,
+ *   logits[i][j][v] = sum_k hidden[i][j][k] * w_vocab[v][k],
+ * accumulated in fp32 and reduced on the fly (they never reach memory).
+ * Only rows j < B_i with masked[i][j] != 0 are projected; other hidden rows
+ * are never read (they may hold NaN).
+ * hidden: [n][L][d] bf16, 16-byte aligned. w_vocab: [V] rows of
+ * w_row_stride bf16 elements (stride >= d, a multiple of 8), 16-byte aligned.
+ * dt must be BS_BF16; d a multiple of 32; L <= 64; q_min >= 1.
+ * tokens, masked, tau, q_min, eos_id and the outputs are as in
+ * bs_parallel_decode (compact [n][L] block state, updated in place).
+ * ws: device workspace of at least bs_lm_head_workspace_bytes(n, L, V)
+ * bytes, 16-byte aligned; contents on entry are ignored (it carries the row
+ * list and partial results between the call's launches). Calls that may
+ * overlap need different workspaces.
+ */
+size_t bs_lm_head_workspace_bytes(int n, int L, int V);
+int bs_lm_head_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int d, int V, bs_dtype dt,
+                      const void* hidden, const void* w_vocab, int64_t w_row_stride, int32_t* tokens,
+                      uint8_t* masked, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
+                      uint8_t* done, uint8_t* eos_seen, float* conf_out, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/*
  * K4 -- KV scatter/compaction at a block boundary (Algorithm 1: completed
  * requests leave and new ones are admitted at the block boundary; Eq. 1
  * discussion: the box shrinks without explicit reclamation; paragraph

@@ -129,6 +129,41 @@ hipError_t launch_decode_marked(const DecArgs& a, bs_dtype dt, hipStream_t s, Ma
   return e;
 }
 
+// ---------------------------------------------------------------- output head
+// Logits of the masked block rows from their hidden states, reduced on the fly
+// into one DecPartial per (row, 128-entry vocabulary slice), then merged into
+// the per-row part the selection reads.
+constexpr int kLmNT = 256;  // vocabulary entries per workgroup tile
+constexpr int kLmMT = 256;  // hidden rows per workgroup tile
+constexpr int kLmKT = 32;   // reduction depth per LDS stage
+constexpr int kLmNS = 4;    // LDS stages
+
+inline int lm_parts(int V) { return 2 * ((V + kLmNT - 1) / kLmNT); }
+
+// Workspace: count (16 B) | row list [n L] int32 | per-row parts [n L]
+// DecPartial | slice parts [n L][lm_parts(V)] DecPartial.
+inline size_t lm_rows_bytes(int n, int L) { return ((size_t)n * L * 4 + 15) / 16 * 16; }
+inline size_t lm_workspace_bytes(int n, int L, int V) {
+  return 16 + lm_rows_bytes(n, L) + (size_t)n * L * sizeof(DecPartial) +
+         (size_t)n * L * lm_parts(V) * sizeof(DecPartial);
+}
+
+struct LmArgs {
+  const bs_req_desc* reqs;
+  int n, L, d, V;
+  const uint16_t* hidden;   // [n][L][d] bf16
+  const uint16_t* w;        // [V][ldw] bf16
+  int64_t ldw;              // elements
+  const uint8_t* masked;    // compact [n][L]
+  int32_t* count;           // masked rows
+  int32_t* rows;            // their compact indices i * L + j, increasing
+  DecPartial* slices;       // [n L][parts]
+  int parts;
+  DecPartial* row_part;     // [n L]: merged, read by the selection
+};
+
+hipError_t launch_lm_head(const LmArgs& a, hipStream_t s);
+
 // ---------------------------------------------------------------- gather / scatter
 constexpr int kMaxGather = 4;  // tensors moved by one gather/scatter launch
 

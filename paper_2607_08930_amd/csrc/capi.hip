@@ -546,6 +546,76 @@ int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
   return finish(c, sl, s, e, "decode launch");
 }
 
+// ------------------------------------------------------------------ K3 with the output head
+size_t bs_lm_head_workspace_bytes(int n, int L, int V) {
+  if (n <= 0 || L <= 0 || V <= 0) return 0;
+  return lm_workspace_bytes(n, L, V);
+}
+
+int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, int V, bs_dtype dt,
+                      const void* hidden, const void* w_vocab, int64_t w_row_stride, int32_t* tokens,
+                      uint8_t* masked, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
+                      uint8_t* done, uint8_t* eos_seen, float* conf_out, void* ws, size_t ws_bytes,
+                      void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  if (n < 0) return fail(c, BS_ERR_INVALID_ARG, "n < 0");
+  if (n > 0 && !reqs) return fail(c, BS_ERR_INVALID_ARG, "reqs is NULL");
+  if (L < 1) return fail(c, BS_ERR_DESCRIPTOR, "L < 1");
+  for (int i = 0; i < n; ++i) {
+    const bs_req_desc& r = reqs[i];
+    const int64_t K = ((int64_t)r.g + L - 1) / L;
+    if (r.p < 0 || r.g < 1 || r.k < 0 || r.k >= K)
+      return fail(c, BS_ERR_DESCRIPTOR, "request %d: p=%d g=%d k=%d invalid for L=%d", i, r.p, r.g, r.k, L);
+  }
+  if (dt != BS_BF16) return fail(c, BS_ERR_UNSUPPORTED, "the output head runs in bf16 only (dt=%d)", (int)dt);
+  if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
+  if (d < kLmKT || d % kLmKT) return fail(c, BS_ERR_UNSUPPORTED, "d=%d must be a positive multiple of %d", d, kLmKT);
+  if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
+  if (w_row_stride < d || w_row_stride % 8)
+    return fail(c, BS_ERR_INVALID_ARG, "w_row_stride %lld must be >= d and a multiple of 8",
+                (long long)w_row_stride);
+  if ((int64_t)n * L > 65536) return fail(c, BS_ERR_UNSUPPORTED, "n * L = %lld exceeds 65536", (long long)n * L);
+  if ((int64_t)kLmNT * w_row_stride * 2 >= (int64_t)1 << 32)
+    return fail(c, BS_ERR_UNSUPPORTED, "w_row_stride too large for 32-bit tile offsets");
+  if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
+  if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
+  const size_t need = bs_lm_head_workspace_bytes(n, L, V);
+  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  if (n == 0) return BS_OK;
+  if (!hidden || !w_vocab || !tokens || !masked || !n_unmasked || !done || !eos_seen)
+    return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) ||
+      !aligned(ws, 16) || (conf_out && !aligned(conf_out, 4)))
+    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (hidden, w_vocab and ws need 16 bytes)");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  int st = upload_reqs(c, s, reqs, n, &sl);
+  if (st) return st;
+  const bs_req_desc* dreqs = static_cast<const bs_req_desc*>(sl->d);
+  char* wsb = static_cast<char*>(ws);
+  LmArgs m{};
+  m.reqs = dreqs;
+  m.n = n; m.L = L; m.d = d; m.V = V;
+  m.hidden = static_cast<const uint16_t*>(hidden);
+  m.w = static_cast<const uint16_t*>(w_vocab);
+  m.ldw = w_row_stride;
+  m.masked = masked;
+  m.count = reinterpret_cast<int32_t*>(wsb);
+  m.rows = reinterpret_cast<int32_t*>(wsb + 16);
+  m.row_part = reinterpret_cast<DecPartial*>(wsb + 16 + lm_rows_bytes(n, L));
+  m.slices = m.row_part + (size_t)n * L;
+  m.parts = lm_parts(V);
+  DecArgs a = decode_args(dreqs, n, L, V, BS_F32, nullptr, V, tau, q_min, eos_id, n_unmasked, done, eos_seen,
+                          conf_out, m.row_part);
+  a.parts = 1;
+  a.tokens = tokens; a.masked = masked;
+  hipError_t e = launch_lm_head(m, s);
+  if (e == hipSuccess) e = launch_decode_select(a, s);
+  return finish(c, sl, s, e, "output-head decode launch");
+}
+
 // ------------------------------------------------------------------ fused step
 int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
                         int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,

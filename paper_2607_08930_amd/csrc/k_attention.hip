@@ -25,6 +25,7 @@
 #include <float.h>
 
 #include "bs_internal.h"
+#include "bs_lds.h"
 
 namespace bs {
 namespace {
@@ -148,8 +149,6 @@ __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
   for (int k = 0; k < 4; ++k) lsum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{p[2 * k], p[2 * k + 1]}, one, lsum, false);
   return lsum;
 }
-typedef __attribute__((address_space(3))) void lds_void;
-
 // XOR swizzle of a row's 16-byte slots. Rows r0..r0+3 (r0 % 4 == 0) differ in
 // bits 1..2, so the transpose reads of 4 consecutive keys x 2 chunks hit 8
 // distinct slots; any 16 consecutive rows get distinct slots for one chunk.
@@ -157,38 +156,6 @@ template <int NCH>
 __device__ inline int swz(int row) {
   const int base = ((row & 3) << 1) | ((row >> 2) & 1);
   return NCH == 16 ? (base | (row & 8)) : base;
-}
-
-__device__ inline uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)p));
-}
-
-// One wave instruction: 64 lanes x 16 bytes, HBM -> LDS block at `lds` (wave-uniform).
-__device__ inline void dma16(uint32_t lds, const void* gptr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
-               "v"(gptr)
-               : "memory");
-}
-__device__ inline uint64_t uniform64(const void* p) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
-  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-// Same, addressed as a wave-uniform base (SGPRs) plus a 32-bit per-lane byte offset.
-__device__ inline void dma16_sv(uint32_t lds, uint64_t base, uint32_t off) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
-               "v"(off), "s"(uniform64(reinterpret_cast<const void*>(base)))
-               : "memory");
-}
-
-// Wait until at most N (compile time) of this wave's vector-memory operations
-// are outstanding. gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
-// vmcnt_hi[15:14]; counts above 63 wait for everything.
-template <int N>
-__device__ inline void wait_vm_c() {
-  constexpr int n = N > 63 ? 0 : N;
-  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // One (request, KV head) item processed by GW waves that share its K/V tiles:

@@ -68,7 +68,19 @@ def test_calls_without_context_fail_before_any_device_work():
                                       None, None, 10, 0, None, 16, None, 1, None, 1, 0.9, 1, -1, None, None,
                                       None, None, None, None, 0, None) == 1
     assert bs.lib.bs_profile_begin(null, 4) == 1
+    assert bs.lib.bs_lm_head_decode(null, None, 0, 8, 64, 10, 0, None, None, 64, None, None, 0.9, 1, -1, None,
+                                    None, None, None, None, 0, None) == 1
     assert "ctx is NULL" in bs.bs_last_error()
+
+
+def test_lm_head_workspace_query():
+    # count (16 B) + row list (n L int32, 16-byte rounded) + one merged part
+    # per row + one part per (row, 128-entry vocabulary slice)
+    parts = 2 * -(-126464 // 256)
+    assert parts == 988
+    assert bs.bs_lm_head_workspace_bytes(32, 32, 126464) == 16 + 4096 + 1024 * 16 + 1024 * parts * 16
+    assert bs.bs_lm_head_workspace_bytes(1, 3, 1) == 16 + 16 + 3 * 16 + 3 * 2 * 16
+    assert bs.bs_lm_head_workspace_bytes(0, 8, 10) == 0
 
 
 def test_workspace_queries():

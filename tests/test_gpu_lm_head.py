@@ -1,0 +1,173 @@
+"""GPU parity of the output-head decoding step (bs_lm_head_decode) against the
+oracle: logits produced from hidden states by the fused MFMA kernel and
+reduced on the fly, then the selection. Small ragged shapes in full, the
+LLaDA-8B (d 4096, V 126464) and Dream-7B (d 3584, V 152064) shapes on seeded
+samples of requests, no-op and poisoned-row cases, argument checks.
+
+The logits are fp32 sums of exact bf16 products on the GPU and exact fp64
+sums in the oracle, so they differ by accumulation rounding (about 1e-5 on
+logits of magnitude 20): confidences agree within LM_CONF_TOL, and a
+position whose two largest oracle logits lie within ARG_GAP may pick either
+id (its request is exempt from the bit-exact token check)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import check_decode, lazy, say
+
+pytestmark = pytest.mark.gpu
+
+LM_CONF_TOL = 2e-4
+ARG_GAP = 1e-3
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    torch, bs, _ = lazy()
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    c = bs.Context(0)
+    yield c
+    c.close()
+
+
+def run_lm(ctx, w, hidden, wv, tok_c, msk_c, tau=None, q_min=None, ldw=None, dev_hidden=None):
+    torch, bs, bstep = lazy()
+    n, d = w.n, wv.shape[1]
+    ldw = d if ldw is None else ldw
+    wpad = np.zeros((wv.shape[0], ldw), np.uint16)
+    wpad[:, :d] = wv
+    dw = bstep.to_device(wpad, "bf16")
+    dh = bstep.to_device(hidden, "bf16") if dev_hidden is None else dev_hidden
+    dt = bstep.to_device(tok_c)
+    dm = bstep.to_device(msk_c)
+    nun = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    done = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
+    eos = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
+    conf = torch.full((n, w.L), float("nan"), dtype=torch.float32, device="cuda")
+    wsb = bs.bs_lm_head_workspace_bytes(n, w.L, w.V)
+    ws = torch.full((max(wsb, 16),), 0xAB, dtype=torch.uint8, device="cuda")
+    bs.bs_lm_head_decode(ctx, w.reqs, w.L, d, w.V, bs.BS_BF16, dh, dw, ldw, dt, dm,
+                         w.tau if tau is None else tau, w.q_min if q_min is None else q_min, w.eos_id,
+                         nun, done, eos, conf, ws, wsb)
+    torch.cuda.synchronize()
+    return dict(tokens=dt.cpu().numpy(), masked=dm.cpu().numpy(), n_unmasked=nun.cpu().numpy(),
+                done=done.cpu().numpy(), eos_seen=eos.cpu().numpy(), conf=conf.cpu().numpy())
+
+
+def near_ties(w, hidden, wv, msk_c, reqs_idx):
+    """Requests with a masked position whose two largest oracle logits are
+    within ARG_GAP (their predicted id is not fixed at fp32 accumulation)."""
+    keys = [(i, j) for i in reqs_idx for j in range(oracle.geometry(w.reqs[i], w.L).B) if msk_c[i, j]]
+    if not keys:
+        return set()
+    lg = oracle.lm_head_logits(np.stack([hidden[i, j] for i, j in keys]), wv, "bf16")
+    top2 = np.sort(lg, axis=1)[:, -2:] if lg.shape[1] > 1 else np.concatenate([lg, lg - 1e9], 1)
+    return {keys[a][0] for a in range(len(keys)) if top2[a, 1] - top2[a, 0] <= ARG_GAP}
+
+
+def lm_case(ctx, w, d, label, sample=None, tau=None, q_min=None, ldw=None):
+    wv = synth.gen_lm_weight(w, d)
+    hidden = synth.gen_lm_hidden(w, wv)
+    tok, msk, blk = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    say(f"[lm head {label}] n={w.n} L={w.L} d={d} V={w.V} masked={int(blk.sum())}")
+    got = run_lm(ctx, w, hidden, wv, tok_c, msk_c, tau=tau, q_min=q_min, ldw=ldw)
+    idx = list(range(w.n)) if sample is None else sample
+    ref = oracle.lm_head_decode(w.reqs, w.L, hidden, wv, tok_c, msk_c, tau=w.tau if tau is None else tau,
+                                q_min=w.q_min if q_min is None else q_min, eos_id=w.eos_id, dtype="bf16",
+                                only=idx)
+    ties = near_ties(w, hidden, wv, msk_c, idx)
+    sub = {k: v[idx] for k, v in ref.items() if isinstance(v, np.ndarray) and len(v) == w.n}
+    gsub = {k: v[idx] for k, v in got.items()}
+    ties_local = {a for a, i in enumerate(idx) if i in ties}
+    nex = check_decode(w, gsub, sub, reqs=w.reqs[idx], tau=tau, label=label, q_min=q_min,
+                       conf_tol=LM_CONF_TOL, also_exempt=ties_local)
+    say(f"  exempt requests: {nex} of {len(idx)} (near ties {len(ties_local)})")
+    # requests outside the sample keep untouched rows beyond their block
+    return got, ref, nex, (hidden, wv, tok_c, msk_c)
+
+
+def test_lm_head_small_ragged(ctx):
+    # V = 1000 (last 256-tile ragged), d = 64 (two K slices), partial blocks, empty prompt
+    w = synth.custom(8, 2, 2, 16, 1000, "bf16", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8], [1, 0, 1, 2, 0], W=40)
+    _, _, nex, _ = lm_case(ctx, w, 64, "small")
+    assert nex <= 1
+
+
+@pytest.mark.parametrize("V,d", [(257, 32), (32017, 4096)])
+def test_lm_head_medium(ctx, V, d):
+    w = synth.custom(32, 2, 2, 16, V, "bf16", list(range(3, 131, 16)), [64] * 8, [0, 1, 0, 1, 1, 0, 1, 0])
+    _, _, nex, _ = lm_case(ctx, w, d, f"V={V} d={d}")
+    assert nex <= 2
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_lm_head_full_size_sampled(ctx, cfg):
+    w = synth.workload(cfg)
+    d = synth.LM_HEAD_DIM[cfg]
+    sample = sorted(np.random.default_rng(70 + cfg).choice(w.n, size=6, replace=False).tolist())
+    _, _, nex, _ = lm_case(ctx, w, d, f"cfg{cfg}", sample=sample)
+    assert nex <= 2
+
+
+def test_lm_head_strided_head_and_quota(ctx):
+    # w rows padded to a longer stride; fixed-quota schedule (threshold disabled)
+    w = synth.custom(16, 2, 2, 16, 3001, "bf16", [7, 40, 0], [32, 48, 17], [1, 0, 1])
+    got, ref, _, inp = lm_case(ctx, w, 96, "ldw=136 quota 3", tau=1.5, q_min=3, ldw=136)
+    msk_c = inp[3]
+    for i, r in enumerate(w.reqs):
+        nm = int(msk_c[i, :oracle.geometry(r, w.L).B].sum())
+        assert got["n_unmasked"][i] == min(nm, 3)
+
+
+def test_lm_head_unread_rows_may_hold_nan(ctx):
+    torch, bs, bstep = lazy()
+    w = synth.custom(8, 2, 2, 16, 700, "bf16", [4, 9], [16, 6], [1, 0])
+    wv = synth.gen_lm_weight(w, 64)
+    hidden = synth.gen_lm_hidden(w, wv)
+    tok, msk, blk = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    a = run_lm(ctx, w, hidden, wv, tok_c, msk_c)
+    poisoned = hidden.copy()
+    for i, r in enumerate(w.reqs):
+        B = oracle.geometry(r, w.L).B
+        for j in range(w.L):
+            if j >= B or not msk_c[i, j]:
+                poisoned[i, j] = synth.BF16_NAN
+    b = run_lm(ctx, w, poisoned, wv, tok_c, msk_c)
+    for key in a:
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+
+
+def test_lm_head_nothing_masked_is_a_noop(ctx):
+    w = synth.custom(8, 2, 2, 16, 300, "bf16", [4, 9], [16, 6], [1, 0])
+    wv = synth.gen_lm_weight(w, 32)
+    hidden = synth.gen_lm_hidden(w, wv)
+    tok_c = np.full((w.n, w.L), 5, np.int32)
+    msk_c = np.zeros((w.n, w.L), np.uint8)
+    got = run_lm(ctx, w, hidden, wv, tok_c, msk_c)
+    assert (got["tokens"] == 5).all() and (got["masked"] == 0).all()
+    assert (got["n_unmasked"] == 0).all() and (got["done"] == 1).all() and (got["conf"] == -1).all()
+
+
+def test_lm_head_rejects(ctx):
+    torch, bs, bstep = lazy()
+    w = synth.custom(8, 2, 2, 16, 300, "bf16", [4], [16], [1])
+    h = torch.zeros((1, 8, 64), dtype=torch.bfloat16, device="cuda")
+    wd = torch.zeros((300, 64), dtype=torch.bfloat16, device="cuda")
+    t = torch.zeros((1, 8), dtype=torch.int32, device="cuda")
+    m = torch.ones((1, 8), dtype=torch.uint8, device="cuda")
+    o = [torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.uint8, device="cuda"),
+         torch.zeros(1, dtype=torch.uint8, device="cuda")]
+    wsb = bs.bs_lm_head_workspace_bytes(1, 8, 300)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
+    for kw, match in [(dict(dt=bs.BS_F32), "UNSUPPORTED"), (dict(d=48), "UNSUPPORTED"),
+                      (dict(ldw=60), "INVALID_ARG"), (dict(ws_bytes=wsb - 16), "WORKSPACE")]:
+        args = dict(dt=bs.BS_BF16, d=64, ldw=64, ws_bytes=wsb)
+        args.update(kw)
+        with pytest.raises(bs.BlockServeError, match=match):
+            bs.bs_lm_head_decode(ctx, w.reqs, 8, args["d"], 300, args["dt"], h, wd, args["ldw"], t, m, 0.9, 1, -1,
+                                 o[0], o[1], o[2], None, ws, args["ws_bytes"])

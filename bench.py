@@ -101,8 +101,9 @@ def cpu_baseline(w, host, budget_s=12.0, max_reps=200):
 
 
 KERNEL_SOURCES = {   # kernel name prefix -> sources whose change voids its counter-derived traffic
-    "k_attn_bf16": ["k_attention.hip", "bs_internal.h"],
+    "k_attn_bf16": ["k_attention.hip", "bs_internal.h", "bs_lds.h"],
     "k_attn_f32": ["k_attention.hip", "bs_internal.h"],
+    "k_lm_head": ["k_lm_head.hip", "bs_internal.h", "bs_lds.h"],
     "k_decode_parts": ["k_decode.hip", "bs_internal.h"],
     "k_decode_select": ["k_decode.hip", "bs_internal.h"],
 }
@@ -223,6 +224,125 @@ class DeviceProvider:
         return [(q[:n], kn[:n], vn[:n]) for q, kn, vn in self.layers], self.logits[:n]
 
 
+def lm_head_bench(args):
+    """The output head fused with the decoding step (bs_lm_head_decode) against
+    the same step unfused: a hipBLASLt GEMM over the masked rows
+    (torch.matmul), its bf16 logits copied into the [n][L] row layout, then
+    bs_parallel_decode. Prints one JSON line."""
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+    from paper_2607_08930_amd import step as bstep
+
+    torch.cuda.set_device(0)
+    w = synth.workload(args.config)
+    d = synth.LM_HEAD_DIM[args.config]
+    print(f"[bench] output head {w.name} d={d} V={w.V}: generating inputs", file=sys.stderr, flush=True)
+    wv = synth.gen_lm_weight(w, d)
+    hidden = synth.gen_lm_hidden(w, wv)
+    tok, msk, blk = synth.gen_state(w)
+    # compact block state (host copy of the active blocks; padding rows zero)
+    tok_c = np.zeros((w.n, w.L), np.int32)
+    msk_c = np.zeros((w.n, w.L), np.uint8)
+    for i, (r, (s0, B, _)) in enumerate(zip(w.reqs, w.spans())):
+        c0 = int(r["off"]) + s0
+        tok_c[i, :B] = tok[int(r["row"]), c0:c0 + B]
+        msk_c[i, :B] = msk[int(r["row"]), c0:c0 + B]
+    R = int(blk.sum())
+    dW = bstep.to_device(wv, "bf16")
+    dH = bstep.to_device(hidden, "bf16")
+    pb = bs.bs_lm_head_pack_bytes(w.V, d)
+    dP = torch.empty(pb // 2, dtype=torch.bfloat16, device="cuda")
+    t0, m0 = bstep.to_device(tok_c), bstep.to_device(msk_c)
+    dt, dm = t0.clone(), m0.clone()
+    nun = torch.empty(w.n, dtype=torch.int32, device="cuda")
+    done = torch.empty(w.n, dtype=torch.uint8, device="cuda")
+    eos = torch.empty(w.n, dtype=torch.uint8, device="cuda")
+    conf = torch.empty((w.n, w.L), dtype=torch.float32, device="cuda")
+    wsb = bs.bs_lm_head_workspace_bytes(w.n, w.L, w.V)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    idx = torch.as_tensor(np.nonzero(blk.reshape(-1))[0], device="cuda")
+    vpad = (w.V + 7) // 8 * 8
+    logits = torch.empty((w.n * w.L, vpad), dtype=torch.bfloat16, device="cuda")
+    dws = bs.bs_decode_workspace_bytes(w.n, w.L, w.V, bs.BS_BF16)
+    dwsb = torch.empty(max(dws, 16), dtype=torch.uint8, device="cuda")
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    ctx = bs.Context(0)
+    stream = torch.cuda.current_stream()
+    bs.bs_lm_head_pack(ctx, dW, d, w.V, d, bs.BS_BF16, dP, pb, stream=stream)    # once per model
+    H2 = dH.view(w.n * w.L, d)
+
+    def fused():
+        bs.bs_lm_head_decode(ctx, w.reqs, w.L, d, w.V, bs.BS_BF16, dH, dP, dt, dm, w.tau, w.q_min, w.eos_id,
+                             nun, done, eos, conf, ws, wsb, stream=stream)
+
+    def gemm():
+        return torch.matmul(H2.index_select(0, idx), dW.t())
+
+    def unfused():
+        logits[idx, :w.V] = gemm()
+        bs.bs_parallel_decode(ctx, w.reqs, w.L, w.V, bs.BS_BF16, logits, vpad, dt, dm, w.tau, w.q_min, w.eos_id,
+                              nun, done, eos, conf, dwsb, dws, stream=stream)
+
+    def timed(fn, k):
+        out = []
+        for _ in range(k):
+            dt.copy_(t0)
+            dm.copy_(m0)
+            flush.sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1))
+        return float(np.median(out))
+
+    for fn in (fused, unfused, gemm):
+        timed(fn, args.warmup)
+    ms = timed(fused, args.steps)
+    ms_unf = timed(unfused, args.steps)
+    ms_gemm = timed(gemm, args.steps)
+    flops = 2.0 * R * d * w.V
+    positions = int(sum(s[1] for s in w.spans()))
+    tflops = flops / (ms / 1e3) / 1e12
+    ctx.close()
+    res = {
+        "metric": "denoised block positions/s per decoding step with the output head",
+        "value": round(positions / (ms / 1e3), 1), "unit": "positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name + f"-lm-head-d{d}", "n_requests": w.n, "masked_rows": R, "d": d, "V": w.V,
+                   "cache": "cold (512 MiB read sweep between steps)"},
+        "unfused_ms": round(ms_unf, 5), "unfused_gemm_ms": round(ms_gemm, 5),
+        "speedup_vs_unfused": round(ms_unf / ms, 3),
+        "roofline": {"kernel": "k_lm_head", "bound": "mfma", "achieved": round(tflops, 1),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(ms, 5),
+                     "note": "whole call (row list, GEMM, merge, selection) timed; the GEMM dominates",
+                     "traffic": read_traffic(w.name + f"-lm-head-d{d}", "k_lm_head")},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        print("[bench] timing the CPU oracle on a sample of the same inputs", file=sys.stderr, flush=True)
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = 1
+        tic, reps, pos = time.perf_counter(), 0, 0
+        while time.perf_counter() - tic < 12.0 and reps < w.n:
+            oracle.lm_head_decode(w.reqs, w.L, hidden, wv, tok_c, msk_c, tau=w.tau, q_min=w.q_min,
+                                  eos_id=w.eos_id, dtype="bf16", only=[reps])
+            pos += w.spans()[reps][1]
+            reps += 1
+        el = time.perf_counter() - tic
+        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"{reps} requests' decoding steps with the output head (fp64), {el:.1f} s"}
+    print(json.dumps(res), flush=True)
+
+
 def serve_bench(args):
     """Closed-loop serving of a stream shaped like one row of the benchmark
     statistics table; prints one JSON line."""
@@ -288,9 +408,18 @@ def main():
     ap.add_argument("--layers", type=int, default=1)
     ap.add_argument("--block-length", type=int, default=None,
                     help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
+    ap.add_argument("--lm-head", action="store_true",
+                    help="time the output head fused with the decoding step against the unfused GEMM + decode")
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
+    if args.lm_head:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        lm_head_bench(args)
+        return
     if args.serve:
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",

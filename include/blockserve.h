@@ -214,10 +214,12 @@ int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V
  * accumulated in fp32 and reduced on the fly (they never reach memory).
  * Only rows j < B_i with masked[i][j] != 0 are projected; other hidden rows
  * are never read (they may hold NaN).
- * hidden: [n][L][d] bf16, 16-byte aligned. w_vocab: [V] rows of
- * w_row_stride bf16 elements (stride >= d, a multiple of 8), 16-byte aligned.
- * dt must be BS_BF16; d a multiple of 32; L <= 64; q_min >= 1.
- * tokens, masked, tau, q_min, eos_id and the outputs are as in
+ * The output-head matrix is passed in the packed layout bs_lm_head_pack
+ * writes (once per model): contiguous 16 KiB slabs that the kernel's LDS
+ * stages copy whole.
+ * hidden: [n][L][d] bf16, 16-byte aligned. w_packed: bs_lm_head_pack's output
+ * for the same V and d. dt must be BS_BF16; d a multiple of 32; L <= 64;
+ * q_min >= 1. tokens, masked, tau, q_min, eos_id and the outputs are as in
  * bs_parallel_decode (compact [n][L] block state, updated in place).
  * ws: device workspace of at least bs_lm_head_workspace_bytes(n, L, V)
  * bytes, 16-byte aligned; contents on entry are ignored (it carries the row
@@ -226,10 +228,23 @@ int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V
  */
 size_t bs_lm_head_workspace_bytes(int n, int L, int V);
 int bs_lm_head_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int d, int V, bs_dtype dt,
-                      const void* hidden, const void* w_vocab, int64_t w_row_stride, int32_t* tokens,
-                      uint8_t* masked, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
-                      uint8_t* done, uint8_t* eos_seen, float* conf_out, void* ws, size_t ws_bytes,
-                      void* stream);
+                      const void* hidden, const void* w_packed, int32_t* tokens, uint8_t* masked, float tau,
+                      int32_t q_min, int32_t eos_id, int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen,
+                      float* conf_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Re-layout of the output-head matrix for bs_lm_head_decode (done once, when
+ * the model is loaded). w_vocab: [V] rows of w_row_stride bf16 elements
+ * (stride >= d, a multiple of 8), 16-byte aligned, read only. w_packed:
+ * device buffer of at least bs_lm_head_pack_bytes(V, d) bytes, 16-byte
+ * aligned, fully written: for each 256-row vocabulary tile t and 32-wide K
+ * slice s, a 16 KiB slab at element offset (t * (d / 32) + s) * 8192 holds
+ * rows 256 t .. 256 t + 255 (zero past V) as 64-byte rows whose 16-byte chunk
+ * c sits in slot c ^ ((row >> 2) & 3). dt must be BS_BF16, d a multiple of 32.
+ */
+size_t bs_lm_head_pack_bytes(int V, int d);
+int bs_lm_head_pack(bs_ctx* ctx, const void* w_vocab, int64_t w_row_stride, int V, int d, bs_dtype dt,
+                    void* w_packed, size_t packed_bytes, void* stream);
 
 /*
  * K4 -- KV scatter/compaction at a block boundary (Algorithm 1: completed

@@ -97,8 +97,10 @@ _SIGS = {
     "bs_parallel_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _f32, _i32, _i32,
                                   _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "bs_lm_head_workspace_bytes": (_sz, [_i32, _i32, _i32]),
-    "bs_lm_head_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _f32, _i32,
-                                 _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bs_lm_head_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _i32, _i32,
+                                 _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bs_lm_head_pack_bytes": (_sz, [_i32, _i32]),
+    "bs_lm_head_pack": (_i32, [_vp, _vp, _i64, _i32, _i32, _i32, _vp, _sz, _vp]),
     "bs_kv_scatter_compact": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp,
                                      _vp, _i64, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp]),
 }
@@ -276,13 +278,22 @@ def bs_lm_head_workspace_bytes(n, L, V) -> int:
     return int(lib.bs_lm_head_workspace_bytes(n, L, V))
 
 
-def bs_lm_head_decode(ctx, reqs, L, d, V, dt, hidden, w_vocab, w_row_stride, tokens, masked, tau, q_min, eos_id,
+def bs_lm_head_decode(ctx, reqs, L, d, V, dt, hidden, w_packed, tokens, masked, tau, q_min, eos_id,
                       n_unmasked, done, eos_seen, conf_out=None, ws=None, ws_bytes=0, stream=None):
     r = _host(reqs, REQ_DTYPE)
     return _check(lib.bs_lm_head_decode(
-        _ptr(ctx), _ptr(r), len(r), L, d, V, dt, _ptr(hidden), _ptr(w_vocab), int(w_row_stride), _ptr(tokens),
-        _ptr(masked), float(tau), int(q_min), int(eos_id), _ptr(n_unmasked), _ptr(done), _ptr(eos_seen),
-        _ptr(conf_out), _ptr(ws), int(ws_bytes), _stream(stream)), ctx)
+        _ptr(ctx), _ptr(r), len(r), L, d, V, dt, _ptr(hidden), _ptr(w_packed), _ptr(tokens), _ptr(masked),
+        float(tau), int(q_min), int(eos_id), _ptr(n_unmasked), _ptr(done), _ptr(eos_seen), _ptr(conf_out),
+        _ptr(ws), int(ws_bytes), _stream(stream)), ctx)
+
+
+def bs_lm_head_pack_bytes(V, d) -> int:
+    return int(lib.bs_lm_head_pack_bytes(V, d))
+
+
+def bs_lm_head_pack(ctx, w_vocab, w_row_stride, V, d, dt, w_packed, packed_bytes, stream=None):
+    return _check(lib.bs_lm_head_pack(_ptr(ctx), _ptr(w_vocab), int(w_row_stride), V, d, dt, _ptr(w_packed),
+                                      int(packed_bytes), _stream(stream)), ctx)
 
 
 def bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt, src_k, src_v, src_layer_stride, R_src, W_src,

@@ -19,23 +19,46 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the HIP library)")
 
 
+# Sources whose MFMA accumulators may live in AGPRs (none at present). The
+# others keep their accumulators in ordinary VGPRs: the attention loop
+# rescales them under a branch, which with AGPR accumulators costs copies
+# every tile.
+AGPR_SOURCES: set[str] = set()
+
+
+def _compile(src: str, obj: str) -> subprocess.CompletedProcess:
+    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-c",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+    if os.path.basename(src) not in AGPR_SOURCES:
+        cmd += ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+    cmd += ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+            "-Wno-unused-command-line-argument", "-o", obj, src]
+    return subprocess.run(cmd, capture_output=True, text=True)
+
+
 def build(verbose: bool = False) -> str:
-    """Always recompiles every source; returns the library path."""
+    """Always recompiles every source (one object each, in parallel, then one
+    link); returns the library path."""
+    import tempfile
+    from concurrent.futures import ThreadPoolExecutor
+
     srcs = sorted(glob.glob(os.path.join(PKG, "csrc", "*.hip")))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           # MFMA accumulators in ordinary VGPRs: the attention loop rescales them
-           # under a branch, which with AGPR accumulators costs copies every tile
-           "-mllvm", "-amdgpu-mfma-vgpr-form",
-           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
-           "-Wno-unused-command-line-argument", "-o", tmp] + srcs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed building libblockserve.so")
+    with tempfile.TemporaryDirectory(prefix="bs_build_") as td:
+        objs = [os.path.join(td, os.path.basename(s) + ".o") for s in srcs]
+        with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+            results = list(ex.map(_compile, srcs, objs))
+        for src, r in zip(srcs, results):
+            if verbose:
+                print("compiled", os.path.basename(src), flush=True)
+            if r.returncode != 0:
+                sys.stderr.write(r.stdout + r.stderr)
+                raise RuntimeError(f"hipcc failed compiling {os.path.basename(src)}")
+        link = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
+        r = subprocess.run(link, capture_output=True, text=True)
+        if r.returncode != 0:
+            sys.stderr.write(r.stdout + r.stderr)
+            raise RuntimeError("hipcc failed linking libblockserve.so")
     os.replace(tmp, LIB)
     return LIB
 

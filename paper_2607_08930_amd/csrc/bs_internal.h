@@ -148,12 +148,18 @@ inline size_t lm_workspace_bytes(int n, int L, int V) {
          (size_t)n * L * lm_parts(V) * sizeof(DecPartial);
 }
 
+// Packed output-head matrix: one 16 KiB slab per (256-row vocabulary tile
+// vt, 32-wide K slice kt), slab (vt, kt) at element (vt * (d / 32) + kt) *
+// 8192, holding rows vt * 256 .. + 256 (rows past V zero) as 64-byte rows
+// whose 16-byte chunk c sits in slot c ^ ((row >> 2) & 3) -- the LDS order,
+// so a stage of the ring is one contiguous copy.
+inline size_t lm_packed_bytes(int V, int d) { return (size_t)((V + kLmNT - 1) / kLmNT) * kLmNT * d * 2; }
+
 struct LmArgs {
   const bs_req_desc* reqs;
   int n, L, d, V;
   const uint16_t* hidden;   // [n][L][d] bf16
-  const uint16_t* w;        // [V][ldw] bf16
-  int64_t ldw;              // elements
+  const uint16_t* w;        // packed (see lm_packed_bytes)
   const uint8_t* masked;    // compact [n][L]
   int32_t* count;           // masked rows
   int32_t* rows;            // their compact indices i * L + j, increasing
@@ -163,6 +169,7 @@ struct LmArgs {
 };
 
 hipError_t launch_lm_head(const LmArgs& a, hipStream_t s);
+hipError_t launch_lm_pack(const uint16_t* w, int64_t ldw, int V, int d, uint16_t* packed, hipStream_t s);
 
 // ---------------------------------------------------------------- gather / scatter
 constexpr int kMaxGather = 4;  // tensors moved by one gather/scatter launch

@@ -552,11 +552,37 @@ size_t bs_lm_head_workspace_bytes(int n, int L, int V) {
   return lm_workspace_bytes(n, L, V);
 }
 
+size_t bs_lm_head_pack_bytes(int V, int d) {
+  if (V <= 0 || d <= 0) return 0;
+  return lm_packed_bytes(V, d);
+}
+
+int bs_lm_head_pack(bs_ctx* c, const void* w_vocab, int64_t w_row_stride, int V, int d, bs_dtype dt,
+                    void* w_packed, size_t packed_bytes, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  if (dt != BS_BF16) return fail(c, BS_ERR_UNSUPPORTED, "the output head runs in bf16 only (dt=%d)", (int)dt);
+  if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
+  if (d < kLmKT || d % kLmKT) return fail(c, BS_ERR_UNSUPPORTED, "d=%d must be a positive multiple of %d", d, kLmKT);
+  if (w_row_stride < d || w_row_stride % 8)
+    return fail(c, BS_ERR_INVALID_ARG, "w_row_stride %lld must be >= d and a multiple of 8",
+                (long long)w_row_stride);
+  if (packed_bytes < lm_packed_bytes(V, d))
+    return fail(c, BS_ERR_WORKSPACE, "packed buffer %zu < %zu bytes", packed_bytes, lm_packed_bytes(V, d));
+  if (!w_vocab || !w_packed) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(w_vocab, 16) || !aligned(w_packed, 16)) return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_lm_pack(static_cast<const uint16_t*>(w_vocab), w_row_stride, V, d,
+                                static_cast<uint16_t*>(w_packed), s);
+  if (e != hipSuccess) return hip_fail(c, e, "output-head pack launch");
+  return BS_OK;
+}
+
 int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, int V, bs_dtype dt,
-                      const void* hidden, const void* w_vocab, int64_t w_row_stride, int32_t* tokens,
-                      uint8_t* masked, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
-                      uint8_t* done, uint8_t* eos_seen, float* conf_out, void* ws, size_t ws_bytes,
-                      void* stream) {
+                      const void* hidden, const void* w_packed, int32_t* tokens, uint8_t* masked, float tau,
+                      int32_t q_min, int32_t eos_id, int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen,
+                      float* conf_out, void* ws, size_t ws_bytes, void* stream) {
   if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
   if (n < 0) return fail(c, BS_ERR_INVALID_ARG, "n < 0");
   if (n > 0 && !reqs) return fail(c, BS_ERR_INVALID_ARG, "reqs is NULL");
@@ -571,22 +597,17 @@ int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, i
   if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
   if (d < kLmKT || d % kLmKT) return fail(c, BS_ERR_UNSUPPORTED, "d=%d must be a positive multiple of %d", d, kLmKT);
   if (V < 1) return fail(c, BS_ERR_INVALID_ARG, "V < 1");
-  if (w_row_stride < d || w_row_stride % 8)
-    return fail(c, BS_ERR_INVALID_ARG, "w_row_stride %lld must be >= d and a multiple of 8",
-                (long long)w_row_stride);
   if ((int64_t)n * L > 65536) return fail(c, BS_ERR_UNSUPPORTED, "n * L = %lld exceeds 65536", (long long)n * L);
-  if ((int64_t)kLmNT * w_row_stride * 2 >= (int64_t)1 << 32)
-    return fail(c, BS_ERR_UNSUPPORTED, "w_row_stride too large for 32-bit tile offsets");
   if (q_min < 1) return fail(c, BS_ERR_INVALID_ARG, "q_min=%d must be >= 1", q_min);
   if (!(tau == tau)) return fail(c, BS_ERR_INVALID_ARG, "tau is NaN");
   const size_t need = bs_lm_head_workspace_bytes(n, L, V);
   if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   if (n == 0) return BS_OK;
-  if (!hidden || !w_vocab || !tokens || !masked || !n_unmasked || !done || !eos_seen)
+  if (!hidden || !w_packed || !tokens || !masked || !n_unmasked || !done || !eos_seen)
     return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
-  if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) ||
+  if (!aligned(hidden, 16) || !aligned(w_packed, 16) || !aligned(tokens, 4) || !aligned(n_unmasked, 4) ||
       !aligned(ws, 16) || (conf_out && !aligned(conf_out, 4)))
-    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (hidden, w_vocab and ws need 16 bytes)");
+    return fail(c, BS_ERR_INVALID_ARG, "misaligned pointer (hidden, w_packed and ws need 16 bytes)");
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -599,8 +620,7 @@ int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, i
   m.reqs = dreqs;
   m.n = n; m.L = L; m.d = d; m.V = V;
   m.hidden = static_cast<const uint16_t*>(hidden);
-  m.w = static_cast<const uint16_t*>(w_vocab);
-  m.ldw = w_row_stride;
+  m.w = static_cast<const uint16_t*>(w_packed);
   m.masked = masked;
   m.count = reinterpret_cast<int32_t*>(wsb);
   m.rows = reinterpret_cast<int32_t*>(wsb + 16);

@@ -6,6 +6,9 @@
 // (max, smallest index attaining it, sum of exp(x - max)) as they leave the
 // matrix cores and are never stored; the selection then runs unchanged.
 //
+// k_lm_pack   once per model: lays the output-head matrix out as the
+//             contiguous 16 KiB slabs the ring stages copy (the [V][d] layout
+//             would read 64 bytes from each of 256 rows 2 d bytes apart).
 // k_lm_rows   one workgroup lists the masked rows (j < B_i, masked) of the
 //             compact [n][L] block state in increasing order and counts them.
 // k_lm_head   C^T = W H^T on v_mfma_f32_32x32x16_bf16 over 256 (vocabulary)
@@ -69,13 +72,31 @@ __global__ __launch_bounds__(512, 1) void k_lm_head(LmArgs a) {
   const int count = *a.count;
   const int nvt = (a.V + kLmNT - 1) / kLmNT;
   const int nrt = (a.n * a.L + kLmMT - 1) / kLmMT;
-  // Workgroups b = x + 8 q run on XCD x; consecutive q on one XCD take the
-  // row tiles of one vocabulary tile, which then share that XCD's L2 copy of
-  // the W slice (W is read from HBM about once).
-  const int total = nvt * nrt, per_xcd = (total + 7) / 8;
-  const int lin = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
-  if (lin >= total) return;
-  const int vt = lin / nrt, rt = lin - vt * nrt;
+  // Workgroups b = x + 8 q run on XCD x. With one or two row tiles in use,
+  // XCD x serves row tile x % nact only: that tile's hidden rows stay in its
+  // L2 while W streams past, and the XCDs serving a row tile split the
+  // vocabulary tiles round-robin (W is read once per row tile). With more
+  // row tiles, consecutive q on one XCD take all row tiles of one vocabulary
+  // tile, which then share that XCD's L2 copy of the W slab (W is read about
+  // once; the hidden rows come from L2 or the Infinity Cache). Measured on
+  // the LLaDA-8B and Dream-7B head shapes, each order is the faster one in
+  // its range.
+  if (count == 0) return;
+  const int x = (int)(blockIdx.x & 7), q = (int)(blockIdx.x >> 3);
+  const int nact = (count + kLmMT - 1) / kLmMT;
+  int vt, rt;
+  if (nact <= 2) {
+    rt = x % nact;
+    const int gsize = (8 - rt + nact - 1) / nact;
+    vt = q * gsize + x / nact;
+    if (vt >= nvt) return;
+  } else {
+    const int total = nvt * nrt, per_xcd = (total + 7) / 8;
+    const int lin = x * per_xcd + q;
+    if (q >= per_xcd || lin >= total) return;
+    vt = lin / nrt;
+    rt = lin - vt * nrt;
+  }
   const int v0 = vt * kLmNT, r0 = rt * kLmMT;
   if (r0 >= count) return;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -87,34 +108,27 @@ __global__ __launch_bounds__(512, 1) void k_lm_head(LmArgs a) {
   const int gch = (lane & 3) ^ ((lane >> 4) & 3);
   const bool wside = w < 4;
   const int b0 = (w & 3) * 4;
-  uint32_t woff[4];                            // W: byte offset from the tile's first row
+  // W comes from the packed slabs (already in LDS order: block b of slab
+  // (vt, t) is one contiguous KiB); H rows are gathered through the row list.
   const uint16_t* hp[4];                       // H: listed row's K start + chunk
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int row = 16 * (b0 + q) + (lane >> 2);
-    if (wside) {
-      const int v = min(v0 + row, a.V - 1);    // rows past V repeat a valid row (masked later)
-      woff[q] = (uint32_t)(((int64_t)(v - v0) * a.ldw + gch * 8) * 2);
-      hp[q] = nullptr;
-    } else {
-      const int x = a.rows[min(r0 + row, count - 1)];
-      hp[q] = a.hidden + (int64_t)x * a.d + gch * 8;
-      woff[q] = 0;
-    }
+    hp[q] = wside ? nullptr : a.hidden + (int64_t)a.rows[min(r0 + row, count - 1)] * a.d + gch * 8;
   }
   const uint32_t ring_lds = lds_addr(ring) + (uint32_t)((wside ? 0 : kTile * 2) + b0 * 1024);
-  const uint16_t* wtile = a.w + (int64_t)v0 * a.ldw;
-  auto issue = [&](int t) {
+  const uint16_t* wslab = a.w + (int64_t)vt * (a.d / kLmKT) * kTile + b0 * 512;
+  // block q of this wave's share of stage t
+  auto issue1 = [&](int t, int q) {
     const uint32_t sb = __builtin_amdgcn_readfirstlane(ring_lds + (uint32_t)((t % kLmNS) * kStage * 2));
-    const int k0 = t * kLmKT;
-    if (wside) {
-      const uint64_t base = uniform64(wtile + k0);
+    if (wside)
+      dma16_sv(sb + q * 1024, uniform64(wslab + (int64_t)t * kTile + q * 512), (uint32_t)(lane * 16));
+    else
+      dma16(sb + q * 1024, hp[q] + t * kLmKT);
+  };
+  auto issue = [&](int t) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dma16_sv(sb + q * 1024, base, woff[q]);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) dma16(sb + q * 1024, hp[q] + k0);
-    }
+    for (int q = 0; q < 4; ++q) issue1(t, q);
   };
 
   // MFMA operands: wave (wv, wr) = (w & 1, w >> 1) computes vocabulary rows
@@ -146,25 +160,34 @@ __global__ __launch_bounds__(512, 1) void k_lm_head(LmArgs a) {
       wait_vm_c<4>();
     else
       wait_vm_c<0>();
-    // after the barrier every wave is done with stage t - 1, whose slot is refilled
+    // after the barrier every wave is done with stage t - 1, whose slot is
+    // refilled: one DMA block after every four MFMAs
     __syncthreads();
-    if (t + kLmNS - 1 < nk) issue(t + kLmNS - 1);
+    const bool refill = t + kLmNS - 1 < nk;
     const uint16_t* st = ring + (t % kLmNS) * kStage;
     const uint16_t* at = st + (128 * wv) * kLmKT;
     const uint16_t* bt = st + kTile + (64 * wr) * kLmKT;
+    bf16x8_t A[2][4], B[2][2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      bf16x8_t A[4], B[2];
 #pragma unroll
-      for (int vb = 0; vb < 4; ++vb) A[vb] = *reinterpret_cast<const bf16x8_t*>(at + 32 * vb * kLmKT + off[s]);
+      for (int vb = 0; vb < 4; ++vb) A[s][vb] = *reinterpret_cast<const bf16x8_t*>(at + 32 * vb * kLmKT + off[s]);
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) B[rb] = *reinterpret_cast<const bf16x8_t*>(bt + 32 * rb * kLmKT + off[s]);
+      for (int rb = 0; rb < 2; ++rb) B[s][rb] = *reinterpret_cast<const bf16x8_t*>(bt + 32 * rb * kLmKT + off[s]);
+    }
 #pragma unroll
-      for (int vb = 0; vb < 4; ++vb)
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb) {
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
-          acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[vb], B[rb], acc[vb][rb], 0, 0, 0);
-    }
+          acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[s][vb], B[s][rb], acc[vb][rb], 0, 0, 0);
+        if (vb & 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (refill) issue1(t + kLmNS - 1, 2 * s + (vb >> 1));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
   }
 
   // Epilogue: lane (g, n) holds C^T[vocab v][row n] for
@@ -261,13 +284,39 @@ __global__ __launch_bounds__(64) void k_lm_merge(LmArgs a) {
   }
 }
 
+// One thread per 16-byte chunk of the packed matrix: slab (vt, kt), row r,
+// slot s holds W[vt * 256 + r][32 kt + 8 (s ^ ((r >> 2) & 3)) .. + 8], or
+// zeros for rows past V.
+__global__ __launch_bounds__(256) void k_lm_pack(const uint16_t* w, int64_t ldw, int V, int d, uint16_t* packed) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;      // chunk index
+  const int nkt = d / kLmKT;
+  const int64_t total = (int64_t)((V + kLmNT - 1) / kLmNT) * nkt * kLmNT * 4;
+  if (x >= total) return;
+  const int slot = (int)(x & 3), r = (int)((x >> 2) & (kLmNT - 1));
+  const int64_t slab = x >> 10;                                     // 1024 chunks per slab
+  const int kt = (int)(slab % nkt), vt = (int)(slab / nkt);
+  const int v = vt * kLmNT + r;
+  v4u val = v4u{0u, 0u, 0u, 0u};
+  if (v < V) val = ld16(w + (int64_t)v * ldw + kt * kLmKT + (slot ^ ((r >> 2) & 3)) * 8);
+  st16(packed + x * 8, val);
+}
+
 }  // namespace
+
+hipError_t launch_lm_pack(const uint16_t* w, int64_t ldw, int V, int d, uint16_t* packed, hipStream_t s) {
+  const int64_t chunks = (int64_t)((V + kLmNT - 1) / kLmNT) * (d / kLmKT) * kLmNT * 4;
+  hipLaunchKernelGGL(k_lm_pack, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, w, ldw, V, d, packed);
+  return hipGetLastError();
+}
 
 hipError_t launch_lm_head(const LmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_rows, dim3(1), dim3(1024), 0, s, a);
   const int nvt = (a.V + kLmNT - 1) / kLmNT;
   const int nrt = (a.n * a.L + kLmMT - 1) / kLmMT;
-  const int per_xcd = (nvt * nrt + 7) / 8;
+  // enough workgroups per XCD for either order: nvt covers the one-row-tile
+  // order (an XCD serves at most nvt vocabulary tiles), the other needs
+  // ceil(nvt * nrt / 8)
+  const int per_xcd = max((nvt * nrt + 7) / 8, nvt);
   hipLaunchKernelGGL(k_lm_head, dim3((unsigned)(8 * per_xcd)), dim3(512), 0, s, a);
   hipLaunchKernelGGL(k_lm_merge, dim3((unsigned)(a.n * a.L)), dim3(64), 0, s, a);
   return hipGetLastError();

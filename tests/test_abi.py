@@ -68,8 +68,9 @@ def test_calls_without_context_fail_before_any_device_work():
                                       None, None, 10, 0, None, 16, None, 1, None, 1, 0.9, 1, -1, None, None,
                                       None, None, None, None, 0, None) == 1
     assert bs.lib.bs_profile_begin(null, 4) == 1
-    assert bs.lib.bs_lm_head_decode(null, None, 0, 8, 64, 10, 0, None, None, 64, None, None, 0.9, 1, -1, None,
+    assert bs.lib.bs_lm_head_decode(null, None, 0, 8, 64, 10, 0, None, None, None, None, 0.9, 1, -1, None,
                                     None, None, None, None, 0, None) == 1
+    assert bs.lib.bs_lm_head_pack(null, None, 64, 10, 64, 0, None, 0, None) == 1
     assert "ctx is NULL" in bs.bs_last_error()
 
 
@@ -81,6 +82,9 @@ def test_lm_head_workspace_query():
     assert bs.bs_lm_head_workspace_bytes(32, 32, 126464) == 16 + 4096 + 1024 * 16 + 1024 * parts * 16
     assert bs.bs_lm_head_workspace_bytes(1, 3, 1) == 16 + 16 + 3 * 16 + 3 * 2 * 16
     assert bs.bs_lm_head_workspace_bytes(0, 8, 10) == 0
+    # packed head: whole 256-row tiles of d bf16 each
+    assert bs.bs_lm_head_pack_bytes(126464, 4096) == 494 * 256 * 4096 * 2
+    assert bs.bs_lm_head_pack_bytes(1, 32) == 256 * 32 * 2
 
 
 def test_workspace_queries():

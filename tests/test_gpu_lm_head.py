@@ -38,6 +38,9 @@ def run_lm(ctx, w, hidden, wv, tok_c, msk_c, tau=None, q_min=None, ldw=None, dev
     wpad = np.zeros((wv.shape[0], ldw), np.uint16)
     wpad[:, :d] = wv
     dw = bstep.to_device(wpad, "bf16")
+    pb = bs.bs_lm_head_pack_bytes(w.V, d)
+    dp = torch.full((pb // 2,), 7, dtype=torch.int16, device="cuda")     # every byte is written by the pack
+    bs.bs_lm_head_pack(ctx, dw, ldw, w.V, d, bs.BS_BF16, dp, pb)
     dh = bstep.to_device(hidden, "bf16") if dev_hidden is None else dev_hidden
     dt = bstep.to_device(tok_c)
     dm = bstep.to_device(msk_c)
@@ -47,7 +50,7 @@ def run_lm(ctx, w, hidden, wv, tok_c, msk_c, tau=None, q_min=None, ldw=None, dev
     conf = torch.full((n, w.L), float("nan"), dtype=torch.float32, device="cuda")
     wsb = bs.bs_lm_head_workspace_bytes(n, w.L, w.V)
     ws = torch.full((max(wsb, 16),), 0xAB, dtype=torch.uint8, device="cuda")
-    bs.bs_lm_head_decode(ctx, w.reqs, w.L, d, w.V, bs.BS_BF16, dh, dw, ldw, dt, dm,
+    bs.bs_lm_head_decode(ctx, w.reqs, w.L, d, w.V, bs.BS_BF16, dh, dp, dt, dm,
                          w.tau if tau is None else tau, w.q_min if q_min is None else q_min, w.eos_id,
                          nun, done, eos, conf, ws, wsb)
     torch.cuda.synchronize()
@@ -103,6 +106,15 @@ def test_lm_head_medium(ctx, V, d):
     assert nex <= 2
 
 
+@pytest.mark.parametrize("n", [22, 60, 90])
+def test_lm_head_row_tile_orders(ctx, n):
+    # 2, 4 and 6 row tiles of 256 masked rows: the one-row-tile-per-XCD order
+    # and the order that keeps all row tiles of a vocabulary tile together
+    w = synth.custom(32, 2, 2, 16, 777, "bf16", [5 + 3 * i for i in range(n)], [64] * n, [i % 2 for i in range(n)])
+    _, _, nex, _ = lm_case(ctx, w, 64, f"n={n} rows")
+    assert nex <= n // 8
+
+
 @pytest.mark.parametrize("cfg", [2, 3])
 def test_lm_head_full_size_sampled(ctx, cfg):
     w = synth.workload(cfg)
@@ -153,6 +165,31 @@ def test_lm_head_nothing_masked_is_a_noop(ctx):
     assert (got["n_unmasked"] == 0).all() and (got["done"] == 1).all() and (got["conf"] == -1).all()
 
 
+def test_lm_head_pack_layout(ctx):
+    # the documented slab layout, checked cell by cell on the host: slab
+    # (t, s) at element (t * (d / 32) + s) * 8192, row r, slot c ^ ((r >> 2) & 3)
+    torch, bs, bstep = lazy()
+    V, d, ldw = 300, 64, 72
+    rng = np.random.default_rng(9)
+    wv = rng.integers(0, 65536, size=(V, ldw), dtype=np.uint16)
+    pb = bs.bs_lm_head_pack_bytes(V, d)
+    assert pb == 2 * 256 * d * 2
+    dp = torch.full((pb // 2,), 7, dtype=torch.int16, device="cuda")
+    bs.bs_lm_head_pack(ctx, bstep.to_device(wv.view(np.int16)), ldw, V, d, bs.BS_BF16, dp, pb)
+    torch.cuda.synchronize()
+    got = dp.cpu().numpy().view(np.uint16)
+    want = np.zeros(pb // 2, np.uint16)
+    for t in range(2):
+        for s in range(d // 32):
+            for r in range(256):
+                v = 256 * t + r
+                for c in range(4):
+                    dst = (t * (d // 32) + s) * 8192 + r * 32 + (c ^ ((r >> 2) & 3)) * 8
+                    if v < V:
+                        want[dst:dst + 8] = wv[v, 32 * s + 8 * c:32 * s + 8 * c + 8]
+    np.testing.assert_array_equal(got, want)
+
+
 def test_lm_head_rejects(ctx):
     torch, bs, bstep = lazy()
     w = synth.custom(8, 2, 2, 16, 300, "bf16", [4], [16], [1])
@@ -164,10 +201,18 @@ def test_lm_head_rejects(ctx):
          torch.zeros(1, dtype=torch.uint8, device="cuda")]
     wsb = bs.bs_lm_head_workspace_bytes(1, 8, 300)
     ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
+    pb = bs.bs_lm_head_pack_bytes(300, 64)
+    wp = torch.zeros(pb // 2, dtype=torch.bfloat16, device="cuda")
     for kw, match in [(dict(dt=bs.BS_F32), "UNSUPPORTED"), (dict(d=48), "UNSUPPORTED"),
-                      (dict(ldw=60), "INVALID_ARG"), (dict(ws_bytes=wsb - 16), "WORKSPACE")]:
-        args = dict(dt=bs.BS_BF16, d=64, ldw=64, ws_bytes=wsb)
+                      (dict(ws_bytes=wsb - 16), "WORKSPACE")]:
+        args = dict(dt=bs.BS_BF16, d=64, ws_bytes=wsb)
         args.update(kw)
         with pytest.raises(bs.BlockServeError, match=match):
-            bs.bs_lm_head_decode(ctx, w.reqs, 8, args["d"], 300, args["dt"], h, wd, args["ldw"], t, m, 0.9, 1, -1,
+            bs.bs_lm_head_decode(ctx, w.reqs, 8, args["d"], 300, args["dt"], h, wp, t, m, 0.9, 1, -1,
                                  o[0], o[1], o[2], None, ws, args["ws_bytes"])
+    for kw, match in [(dict(ldw=60), "INVALID_ARG"), (dict(d=48), "UNSUPPORTED"), (dict(dt=bs.BS_F32), "UNSUPPORTED"),
+                      (dict(pb=pb - 16), "WORKSPACE")]:
+        args = dict(ldw=64, d=64, dt=bs.BS_BF16, pb=pb)
+        args.update(kw)
+        with pytest.raises(bs.BlockServeError, match=match):
+            bs.bs_lm_head_pack(ctx, wd, args["ldw"], 300, args["d"], args["dt"], wp, args["pb"])

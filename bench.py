@@ -157,10 +157,11 @@ def traffic_summary(args, workload):
     lines = [f"# Measured HBM traffic per launch: {workload}", "",
              "Commands (repo root as `$R`, one MI355X; the bench adds one 256 MiB device copy as the",
              "calibration kernel):", "", "```", "cd /tmp && export TMPDIR=/tmp"]
+    mode = " --lm-head" if args.lm_head else ""
     for c, d in (("FETCH_SIZE", args.traffic_summary[0]), ("WRITE_SIZE", args.traffic_summary[1])):
         lines.append(f"rocprofv3 --pmc {c} -d {d} -o run --output-format csv -- "
-                     f"python3 $R/bench.py --config {args.config} --steps 5 --warmup 1 --no-cpu-baseline --pmc-calibration")
-    lines += [f"python3 $R/bench.py --config {args.config} --traffic-summary <fetch dir> <write dir>", "```", "",
+                     f"python3 $R/bench.py{mode} --config {args.config} --steps 5 --warmup 1 --no-cpu-baseline --pmc-calibration")
+    lines += [f"python3 $R/bench.py{mode} --config {args.config} --traffic-summary <fetch dir> <write dir>", "```", "",
               f"Calibration (256 MiB copy): FETCH_SIZE reads {cal_f:.0f} KiB (scale x{kf:.3f}), "
               f"WRITE_SIZE reads {cal_w:.0f} KiB (scale x{kw:.3f}).", "",
               "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | read bytes | written bytes | total bytes |",
@@ -269,6 +270,12 @@ def lm_head_bench(args):
     flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
     ctx = bs.Context(0)
     stream = torch.cuda.current_stream()
+    if args.pmc_calibration:
+        src_ = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst_ = torch.empty_like(src_)
+        dst_.copy_(src_)
+        torch.cuda.synchronize()
+        del src_, dst_
     bs.bs_lm_head_pack(ctx, dW, d, w.V, d, bs.BS_BF16, dP, pb, stream=stream)    # once per model
     H2 = dH.view(w.n * w.L, d)
 
@@ -300,12 +307,15 @@ def lm_head_bench(args):
 
     for fn in (fused, unfused, gemm):
         timed(fn, args.warmup)
+    bs.bs_profile_begin(ctx, args.steps)          # phases of every fused call: row list | GEMM | merge + select
     ms = timed(fused, args.steps)
+    ph = bs.bs_profile_end(ctx, args.steps)
+    gemm_ms = float(np.median(ph[:, 1]))
     ms_unf = timed(unfused, args.steps)
     ms_gemm = timed(gemm, args.steps)
     flops = 2.0 * R * d * w.V
     positions = int(sum(s[1] for s in w.spans()))
-    tflops = flops / (ms / 1e3) / 1e12
+    tflops = flops / (gemm_ms / 1e3) / 1e12
     ctx.close()
     res = {
         "metric": "denoised block positions/s per decoding step with the output head",
@@ -316,10 +326,11 @@ def lm_head_bench(args):
                    "cache": "cold (512 MiB read sweep between steps)"},
         "unfused_ms": round(ms_unf, 5), "unfused_gemm_ms": round(ms_gemm, 5),
         "speedup_vs_unfused": round(ms_unf / ms, 3),
+        "phases_ms": {"rows": round(float(np.median(ph[:, 0])), 5), "gemm": round(gemm_ms, 5),
+                      "merge_select": round(float(np.median(ph[:, 2])), 5)},
         "roofline": {"kernel": "k_lm_head", "bound": "mfma", "achieved": round(tflops, 1),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(ms, 5),
-                     "note": "whole call (row list, GEMM, merge, selection) timed; the GEMM dominates",
+                     "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(gemm_ms, 5),
                      "traffic": read_traffic(w.name + f"-lm-head-d{d}", "k_lm_head")},
     }
     if not args.no_cpu_baseline:
@@ -413,7 +424,7 @@ def main():
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
-    if args.lm_head:
+    if args.lm_head and not args.traffic_summary:
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
                   file=sys.stderr, flush=True)
@@ -430,6 +441,8 @@ def main():
     if args.traffic_summary:
         import synth
         name = synth.workload(args.config, block_length=args.block_length).name
+        if args.lm_head:
+            name += f"-lm-head-d{synth.LM_HEAD_DIM[args.config]}"
         traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
         return
     if args.gpus != 1:

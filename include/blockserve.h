@@ -298,14 +298,16 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
                         size_t ws_bytes, void* stream);
 
 /*
- * Phase timing of bs_mixed_state_step (a trace facility; no method content).
- * bs_profile_begin arms a ring of max_steps steps: each following step call
- * records BS_PROFILE_PHASES + 1 HIP events on its stream (before attention,
- * after attention, after the decode row reductions, after the selection),
- * until max_steps steps are recorded. bs_profile_end waits for the recorded
- * events and writes phase_ms[k][ph] (k < *n_steps, ph < BS_PROFILE_PHASES:
- * attention over all layers, decode row reductions, selection) for up to
- * max_steps steps, then disarms. Events are created once and reused.
+ * Phase timing of bs_mixed_state_step and bs_lm_head_decode (a trace
+ * facility; no method content). bs_profile_begin arms a ring of max_steps
+ * calls: each following call of either entry point records
+ * BS_PROFILE_PHASES + 1 HIP events on its stream, until max_steps calls are
+ * recorded. For bs_mixed_state_step the phases are attention over all
+ * layers, decode row reductions, selection; for bs_lm_head_decode they are
+ * the masked-row list, the output-head GEMM with its on-the-fly reduction,
+ * and the merge plus selection. bs_profile_end waits for the recorded events
+ * and writes phase_ms[k][ph] (k < *n_steps, ph < BS_PROFILE_PHASES) for up to
+ * max_steps calls, then disarms. Events are created once and reused.
  */
 #define BS_PROFILE_PHASES 3
 int bs_profile_begin(bs_ctx* ctx, int max_steps);

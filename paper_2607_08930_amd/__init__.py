@@ -322,7 +322,8 @@ def bs_mixed_state_step(ctx, reqs, L, R, W, layers, Hq, Hkv, D, dt, scale, write
                                           _ptr(conf_out), _ptr(pos_out), _ptr(ws), ws_bytes, _stream(stream)), ctx)
 
 
-PROFILE_PHASES = ("attention", "decode_rows", "decode_select")
+PROFILE_PHASES = ("attention", "decode_rows", "decode_select")          # bs_mixed_state_step
+LM_PROFILE_PHASES = ("rows", "gemm", "merge_select")                      # bs_lm_head_decode
 
 
 def bs_profile_begin(ctx, max_steps: int) -> None:

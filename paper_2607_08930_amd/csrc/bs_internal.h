@@ -168,7 +168,9 @@ struct LmArgs {
   DecPartial* row_part;     // [n L]: merged, read by the selection
 };
 
-hipError_t launch_lm_head(const LmArgs& a, hipStream_t s);
+hipError_t launch_lm_rows(const LmArgs& a, hipStream_t s);
+hipError_t launch_lm_gemm(const LmArgs& a, hipStream_t s);
+hipError_t launch_lm_merge(const LmArgs& a, hipStream_t s);
 hipError_t launch_lm_pack(const uint16_t* w, int64_t ldw, int V, int d, uint16_t* packed, hipStream_t s);
 
 // ---------------------------------------------------------------- gather / scatter

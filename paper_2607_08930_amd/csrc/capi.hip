@@ -631,8 +631,16 @@ int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, i
                           conf_out, m.row_part);
   a.parts = 1;
   a.tokens = tokens; a.masked = masked;
-  hipError_t e = launch_lm_head(m, s);
+  // phase events (when the ring is armed): row list | GEMM | merge + selection
+  hipError_t e = prof_mark(c, 0, s);
+  if (e == hipSuccess) e = launch_lm_rows(m, s);
+  if (e == hipSuccess) e = prof_mark(c, 1, s);
+  if (e == hipSuccess) e = launch_lm_gemm(m, s);
+  if (e == hipSuccess) e = prof_mark(c, 2, s);
+  if (e == hipSuccess) e = launch_lm_merge(m, s);
   if (e == hipSuccess) e = launch_decode_select(a, s);
+  if (e == hipSuccess) e = prof_mark(c, 3, s);
+  if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;
   return finish(c, sl, s, e, "output-head decode launch");
 }
 

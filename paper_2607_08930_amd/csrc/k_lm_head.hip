@@ -309,8 +309,12 @@ hipError_t launch_lm_pack(const uint16_t* w, int64_t ldw, int V, int d, uint16_t
   return hipGetLastError();
 }
 
-hipError_t launch_lm_head(const LmArgs& a, hipStream_t s) {
+hipError_t launch_lm_rows(const LmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_rows, dim3(1), dim3(1024), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_gemm(const LmArgs& a, hipStream_t s) {
   const int nvt = (a.V + kLmNT - 1) / kLmNT;
   const int nrt = (a.n * a.L + kLmMT - 1) / kLmMT;
   // enough workgroups per XCD for either order: nvt covers the one-row-tile
@@ -318,6 +322,10 @@ hipError_t launch_lm_head(const LmArgs& a, hipStream_t s) {
   // ceil(nvt * nrt / 8)
   const int per_xcd = max((nvt * nrt + 7) / 8, nvt);
   hipLaunchKernelGGL(k_lm_head, dim3((unsigned)(8 * per_xcd)), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_merge(const LmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_merge, dim3((unsigned)(a.n * a.L)), dim3(64), 0, s, a);
   return hipGetLastError();
 }

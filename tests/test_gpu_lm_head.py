@@ -165,6 +165,23 @@ def test_lm_head_nothing_masked_is_a_noop(ctx):
     assert (got["n_unmasked"] == 0).all() and (got["done"] == 1).all() and (got["conf"] == -1).all()
 
 
+def test_lm_head_phase_ring(ctx):
+    # the profiling ring records the call's three phases (row list, GEMM,
+    # merge + selection) and stops at its capacity
+    torch, bs, bstep = lazy()
+    w = synth.custom(8, 2, 2, 16, 1000, "bf16", [4, 9], [16, 6], [1, 0])
+    wv = synth.gen_lm_weight(w, 64)
+    hidden = synth.gen_lm_hidden(w, wv)
+    tok, msk, _ = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    bs.bs_profile_begin(ctx, 2)
+    for _ in range(3):
+        run_lm(ctx, w, hidden, wv, tok_c, msk_c)
+    ph = bs.bs_profile_end(ctx, 2)
+    assert ph.shape == (2, len(bs.LM_PROFILE_PHASES)) and (ph > 0).all()
+
+
 def test_lm_head_pack_layout(ctx):
     # the documented slab layout, checked cell by cell on the host: slab
     # (t, s) at element (t * (d / 32) + s) * 8192, row r, slot c ^ ((r >> 2) & 3)

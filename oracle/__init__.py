@@ -33,6 +33,10 @@ decode     confidence-aware parallel decoding with greedy (temperature 0)
            mixed-schedule execution"; "Implementation details").
 lm_head    the same decoding step with its logits produced by the output head
            from the positions' hidden states (logits never stored).
+refresh    the full-row attention of the dual-cache refresh at a block start
+           (and the prefill of newly admitted rows), with rotary embedding at
+           the explicit position ids of paragraph "Logical positional
+           alignment"; the refreshed cache holds the rotated keys.
 compact    KV scatter/compaction when requests are evicted and admitted at a
            block boundary (Algorithm 1; Eq. 1 discussion of the bounding box
            shrinking without explicit reclamation).
@@ -50,6 +54,7 @@ from .gather import gather_active_blocks, scatter_active_blocks
 from .attention import dual_cache_block_attention, attention_rows
 from .decode import parallel_decode, row_stats
 from .lm_head import lm_head_logits, lm_head_decode
+from .refresh import rope, row_positions, dual_cache_refresh
 from .compact import kv_scatter_compact
 from .step import mixed_state_step
 from . import schedule
@@ -59,6 +64,6 @@ __all__ = [
     "geometry", "validate_reqs", "bbox_cost", "position_ids", "transfer_schedule",
     "effective_compute_ratio", "widen", "gather_active_blocks", "scatter_active_blocks",
     "dual_cache_block_attention", "attention_rows", "parallel_decode", "row_stats",
-    "lm_head_logits", "lm_head_decode",
+    "lm_head_logits", "lm_head_decode", "rope", "row_positions", "dual_cache_refresh",
     "kv_scatter_compact", "mixed_state_step",
 ]

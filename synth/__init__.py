@@ -555,3 +555,39 @@ def gen_lm_hidden(w: Workload, wv: np.ndarray) -> np.ndarray:
             h[j] += (math.log(V) + 0.5 + m[j] - h[j] @ wt) / (wt @ wt) * wt
         out[i] = f32_to_bf16_bits(h.astype(np.float32))
     return out
+
+
+# ---------------------------------------------------------------- dual-cache refresh
+S_RQ, S_RK, S_RV = 32, 33, 34
+# rotary bases of the workloads' model shapes (LLaDA-8B: 5e5, Dream-7B: 1e6)
+ROPE_BASE = {1: 10000.0, 2: 500000.0, 3: 1000000.0, 4: 1000000.0, 5: 500000.0}
+
+
+def gen_refresh_row(w: Workload, layer: int, row: int):
+    """Projections of one dense row for the refresh forward, token-major:
+    q [W][Hq][D], k and v [W][Hkv][D] (fp32 values or bf16 bits). Padding
+    cells are drawn too; ``gen_refresh`` can poison them."""
+    q = _normal(rng(w.cfg, w.variant, S_RQ, layer, row), (w.W, w.Hq, w.D), w.q_sigma)
+    k = _normal(rng(w.cfg, w.variant, S_RK, layer, row), (w.W, w.Hkv, w.D), w.kv_sigma)
+    v = _normal(rng(w.cfg, w.variant, S_RV, layer, row), (w.W, w.Hkv, w.D), w.kv_sigma)
+    return _cast(w, q), _cast(w, k), _cast(w, v)
+
+
+def gen_refresh(w: Workload, layer: int = 0, poison: bool = True):
+    """Box projections q [R][W][Hq][D], k/v [R][W][Hkv][D]; with ``poison``
+    every cell outside the requests' logical rows holds NaN."""
+    dt = np.float32 if w.dtype == "f32" else np.uint16
+    q = np.zeros((w.R, w.W, w.Hq, w.D), dt)
+    k = np.zeros((w.R, w.W, w.Hkv, w.D), dt)
+    v = np.zeros_like(k)
+    for row in range(w.R):
+        q[row], k[row], v[row] = gen_refresh_row(w, layer, row)
+    if poison:
+        nanv = np.float32("nan") if w.dtype == "f32" else BF16_NAN
+        used = np.zeros((w.R, w.W), bool)
+        for r in w.reqs:
+            used[int(r["row"]), int(r["off"]):int(r["off"]) + int(r["p"]) + int(r["g"])] = True
+        q[~used] = nanv
+        k[~used] = nanv
+        v[~used] = nanv
+    return q, k, v

@@ -16,6 +16,7 @@ import test_oracle_compact_step as TC
 import test_oracle_decode as TD
 import test_oracle_geometry as TG
 import test_oracle_lm_head as TL
+import test_oracle_refresh as TR
 import test_schedule as TS
 
 
@@ -46,6 +47,7 @@ GEO = "oracle.geometry"
 CMP = "oracle.compact"
 SCH = "oracle.schedule"
 LMH = "oracle.lm_head"
+RFR = "oracle.refresh"
 
 MUTANTS = [
     # (module, anchor, replacement, exported name, pin tests that must catch it)
@@ -117,6 +119,26 @@ MUTANTS = [
     (LMH, "out[:, v0:v0 + chunk] = h @ widen(w_vocab[v0:v0 + chunk], dtype).T",
      "out[:, v0:v0 + chunk] = h @ widen(w_vocab[v0:v0 + chunk][::-1], dtype).T", "lm_head_decode",
      [(TL.test_identity_head_gives_softmax_of_the_hidden_state,)]),
+    (RFR, "x1 * c - x2 * s", "x1 * c + x2 * s", "rope", [(TR.test_rope_two_features_is_a_plane_rotation,)]),
+    (RFR, "x1, x2 = x[..., :half], x[..., half:]", "x1, x2 = x[..., 0::2], x[..., 1::2]", "rope",
+     [(TR.test_rope_pairs_feature_f_with_f_plus_half,)]),
+    (RFR, "inv_freq = float(base) ** (-2.0 * f / D)", "inv_freq = float(base) ** (-1.0 * f / D)", "rope",
+     [(TR.test_rope_pairs_feature_f_with_f_plus_half,), (TR.test_rope_equals_complex_multiplication,)]),
+    (RFR, "return position_ids(mask)[off:off + ln]", "return np.arange(off, off + ln)", "dual_cache_refresh",
+     [(TR.test_placement_in_the_box_does_not_matter,)]),
+    (RFR, "qr = rope(widen(q[row, off:off + ln], dtype), pos[:, None], rope_base)",
+     "qr = widen(q[row, off:off + ln], dtype)", "dual_cache_refresh",
+     [(TR.test_block_rows_match_block_attention_on_the_refreshed_cache,)]),
+    (RFR, "vv = widen(v[row, off:off + ln], dtype)",
+     "vv = rope(widen(v[row, off:off + ln], dtype), pos[:, None], rope_base)", "dual_cache_refresh",
+     [(TR.test_uniform_values_and_one_token_row,)]),
+    (RFR, "kc[row, c, off:off + ln] = kr[:, c]", "kc[row, c, off:off + ln] = widen(k[row, off:off + ln, c], dtype)",
+     "dual_cache_refresh", [(TR.test_block_rows_match_block_attention_on_the_refreshed_cache,)]),
+    (RFR, "c = h // G", "c = h % Hkv", "dual_cache_refresh", [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
+    (RFR, "scale = 1.0 / math.sqrt(D)", "scale = 1.0 / D", "dual_cache_refresh",
+     [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
+    (RFR, "kr = rope(widen(k[row, off:off + ln], dtype)", "kr = rope(widen(k[row, off + 1:off + ln + 1], dtype)",
+     "dual_cache_refresh", [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
 ]
 
 

@@ -104,6 +104,8 @@ KERNEL_SOURCES = {   # kernel name prefix -> sources whose change voids its coun
     "k_attn_bf16": ["k_attention.hip", "bs_internal.h", "bs_lds.h"],
     "k_attn_f32": ["k_attention.hip", "bs_internal.h"],
     "k_lm_head": ["k_lm_head.hip", "bs_internal.h", "bs_lds.h"],
+    "k_refresh_attn": ["k_refresh.hip", "bs_refresh.h", "bs_internal.h", "bs_lds.h"],
+    "k_refresh_kv": ["k_refresh.hip", "bs_refresh.h", "bs_internal.h"],
     "k_decode_parts": ["k_decode.hip", "bs_internal.h"],
     "k_decode_select": ["k_decode.hip", "bs_internal.h"],
 }
@@ -157,7 +159,7 @@ def traffic_summary(args, workload):
     lines = [f"# Measured HBM traffic per launch: {workload}", "",
              "Commands (repo root as `$R`, one MI355X; the bench adds one 256 MiB device copy as the",
              "calibration kernel):", "", "```", "cd /tmp && export TMPDIR=/tmp"]
-    mode = " --lm-head" if args.lm_head else ""
+    mode = " --lm-head" if args.lm_head else (" --refresh" if args.refresh else "")
     for c, d in (("FETCH_SIZE", args.traffic_summary[0]), ("WRITE_SIZE", args.traffic_summary[1])):
         lines.append(f"rocprofv3 --pmc {c} -d {d} -o run --output-format csv -- "
                      f"python3 $R/bench.py{mode} --config {args.config} --steps 5 --warmup 1 --no-cpu-baseline --pmc-calibration")
@@ -354,6 +356,133 @@ def lm_head_bench(args):
     print(json.dumps(res), flush=True)
 
 
+def refresh_bench(args):
+    """The dual-cache refresh of one layer (bs_dual_cache_refresh: rotated keys
+    and values into the cache, then full-row attention) over the whole box of
+    a workload, beside torch's flash attention (SDPA, flash backend only) run
+    one request at a time on the same rotated inputs. Prints one JSON line."""
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+    from paper_2607_08930_amd import step as bstep
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    torch.cuda.set_device(0)
+    w = synth.workload(args.config)
+    base = synth.ROPE_BASE[args.config]
+    print(f"[bench] refresh {w.name}: generating the box projections", file=sys.stderr, flush=True)
+    q, k, v = synth.gen_refresh(w)
+    dq, dk, dv = (bstep.to_device(x, "bf16") for x in (q, k, v))
+    dkc = torch.zeros((w.R, w.Hkv, w.W, w.D), dtype=torch.bfloat16, device="cuda")
+    dvc = torch.zeros_like(dkc)
+    out = torch.zeros_like(dq)
+    lens = [int(r["p"] + r["g"]) for r in w.reqs]
+    flops = float(sum(4.0 * ln * ln * w.D * w.Hq for ln in lens))     # Q K^T and P V, 2 flops per MAC
+    positions = int(sum(lens))
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    ctx = bs.Context(0)
+    stream = torch.cuda.current_stream()
+    if args.pmc_calibration:
+        src_ = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst_ = torch.empty_like(src_)
+        dst_.copy_(src_)
+        torch.cuda.synchronize()
+        del src_, dst_
+
+    def fused():
+        bs.bs_dual_cache_refresh(ctx, w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 0.0, base, dq, dk, dv, w.R, w.W,
+                                 dkc, dvc, out, stream=stream)
+
+    # library comparison: per request, the queries [Hq][len][D] and the cached
+    # (rotated) K/V expanded to the query heads, contiguous; the rotation of the
+    # queries changes no work, so the unrotated ones stand in for them
+    G = w.Hq // w.Hkv
+    lib_in = []
+
+    def prep_library():
+        fused()
+        torch.cuda.synchronize()
+        for r, ln in zip(w.reqs, lens):
+            row, off = int(r["row"]), int(r["off"])
+            kk = dkc[row, :, off:off + ln].repeat_interleave(G, 0).contiguous()
+            vv = dvc[row, :, off:off + ln].repeat_interleave(G, 0).contiguous()
+            qq = dq[row, off:off + ln].transpose(0, 1).contiguous()
+            lib_in.append((qq.unsqueeze(0), kk.unsqueeze(0), vv.unsqueeze(0)))
+
+    def library():
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            for qq, kk, vv in lib_in:
+                torch.nn.functional.scaled_dot_product_attention(qq, kk, vv)
+
+    def timed(fn, kreps):
+        res = []
+        for _ in range(kreps):
+            flush.sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            res.append(e0.elapsed_time(e1))
+        return float(np.median(res))
+
+    timed(fused, args.warmup)
+    bs.bs_profile_begin(ctx, args.steps)          # phases of every call: rotated K/V scatter | attention
+    ms = timed(fused, args.steps)
+    ph = bs.bs_profile_end(ctx, args.steps)
+    kv_ms, att_ms = float(np.median(ph[:, 0])), float(np.median(ph[:, 1]))
+    lib_ms = None
+    if not args.no_library:
+        try:
+            prep_library()
+            timed(library, max(1, args.warmup))
+            lib_ms = timed(library, args.steps)
+        except RuntimeError as e:                 # no flash kernel for this shape on this build
+            print(f"[bench] library flash attention unavailable: {e}", file=sys.stderr, flush=True)
+    ctx.close()
+    tflops = flops / (att_ms / 1e3) / 1e12
+    kv_bytes = float(sum(ln * w.Hkv * w.D * 2 * 4 for ln in lens))   # K and V read once, written once
+    res = {
+        "metric": "refreshed positions/s per layer (dual-cache refresh)",
+        "value": round(positions / (ms / 1e3), 1), "unit": "positions/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name + "-refresh", "n_requests": w.n, "positions": positions, "rope_base": base,
+                   "cache": "cold (512 MiB read sweep between steps)"},
+        "phases_ms": {"rope_kv": round(kv_ms, 5), "attention": round(att_ms, 5)},
+        "rope_kv_GBps": round(kv_bytes / (kv_ms / 1e3) / 1e9, 1),
+        "library_flash_attention_ms": None if lib_ms is None else round(lib_ms, 5),
+        "attention_speedup_vs_library": None if lib_ms is None else round(lib_ms / att_ms, 3),
+        "roofline": {"kernel": "k_refresh_attn", "bound": "mfma", "achieved": round(tflops, 1),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(att_ms, 5),
+                     "traffic": read_traffic(w.name + "-refresh", "k_refresh_attn")},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        print("[bench] timing the CPU oracle on a sample of the same inputs", file=sys.stderr, flush=True)
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = 1
+        order = np.argsort(lens)                  # shortest rows first: several requests fit the budget
+        tic, reps, pos = time.perf_counter(), 0, 0
+        while time.perf_counter() - tic < 12.0 and reps < w.n:
+            i = int(order[reps])
+            r = w.reqs[i]
+            row = int(r["row"])
+            oracle.refresh_row(r, q[row], k[row], v[row], dtype="bf16", rope_base=base)
+            pos += lens[i]
+            reps += 1
+        el = time.perf_counter() - tic
+        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"the {reps} shortest requests' full-row refresh, all heads (fp64), "
+                                         f"{el:.1f} s"}
+    print(json.dumps(res), flush=True)
+
+
 def serve_bench(args):
     """Closed-loop serving of a stream shaped like one row of the benchmark
     statistics table; prints one JSON line."""
@@ -421,6 +550,9 @@ def main():
                     help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
     ap.add_argument("--lm-head", action="store_true",
                     help="time the output head fused with the decoding step against the unfused GEMM + decode")
+    ap.add_argument("--refresh", action="store_true",
+                    help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer")
+    ap.add_argument("--no-library", action="store_true", help="--refresh: skip the library attention comparison")
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
@@ -430,6 +562,13 @@ def main():
                   file=sys.stderr, flush=True)
             sys.exit(2)
         lm_head_bench(args)
+        return
+    if args.refresh and not args.traffic_summary:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        refresh_bench(args)
         return
     if args.serve:
         if args.gpus != 1:
@@ -443,6 +582,8 @@ def main():
         name = synth.workload(args.config, block_length=args.block_length).name
         if args.lm_head:
             name += f"-lm-head-d{synth.LM_HEAD_DIM[args.config]}"
+        if args.refresh:
+            name += "-refresh"
         traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
         return
     if args.gpus != 1:

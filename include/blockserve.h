@@ -247,6 +247,38 @@ int bs_lm_head_pack(bs_ctx* ctx, const void* w_vocab, int64_t w_row_stride, int 
                     void* w_packed, size_t packed_bytes, void* stream);
 
 /*
+ * Dual-cache refresh of one layer at a block start, and the prefill of newly
+ * admitted rows (the dual cache of Fast-dLLM that the paper integrates:
+ * cached prefix and masked-suffix KV are recomputed by a forward over the
+ * whole row when a block starts, Sections "Experimental setup" and "Diffusion
+ * LLM Inference Optimization"; paragraph "Logical positional alignment":
+ * position ids count the real tokens of the left-padded row, so rotary
+ * embeddings see each request's own distances).
+ * For request i (row r, offset off, logical length len = p + g), cell
+ * t < len and position id t (the cumulative count over the row's attention
+ * mask, minus one):
+ *   K_t = rope(k[r][off + t], t),  Q_t = rope(q[r][off + t], t)
+ *   k_cache[r][c][off + t] = K_t,c,  v_cache[r][c][off + t] = v[r][off + t][c]
+ *   out[r][off + t][h] = softmax(scale * Q_t,h . K_c^T) V_c over keys t' < len
+ * (bidirectional; query head h reads KV head c = h / (Hq / Hkv)).
+ * rope(x, t) turns feature pair (f, f + D/2), f < D/2, by the angle
+ * t * rope_base^(-2 f / D) (RoFormer; the rotate-half pairing); rope_base
+ * <= 0 disables the rotation. scale <= 0 selects 1/sqrt(D).
+ * Layouts (bf16): q, out [R][W][Hq][D] and k, v [R][W][Hkv][D] (token-major
+ * projections of the dense box); k_cache, v_cache [R][Hkv][W][D]. Only the
+ * requests' logical cells are read (padding may hold NaN) or written (every
+ * other cell of out and the caches is left unchanged). q, k, v must not
+ * overlap the caches or out. The descriptors are validated as everywhere
+ * (L and k only there); R * W * Hq < 2^31.
+ * Supported: dt = BS_BF16, D = 128, Hq % Hkv == 0. All pointers 16-byte
+ * aligned. Two launches on `stream` (keys and values, then attention).
+ */
+int bs_dual_cache_refresh(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
+                          bs_dtype dt, float scale, float rope_base, const void* q, const void* k,
+                          const void* v, int R, int W, void* k_cache, void* v_cache, void* out,
+                          void* stream);
+
+/*
  * K4 -- KV scatter/compaction at a block boundary (Algorithm 1: completed
  * requests leave and new ones are admitted at the block boundary; Eq. 1
  * discussion: the box shrinks without explicit reclamation; paragraph
@@ -298,14 +330,16 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
                         size_t ws_bytes, void* stream);
 
 /*
- * Phase timing of bs_mixed_state_step and bs_lm_head_decode (a trace
- * facility; no method content). bs_profile_begin arms a ring of max_steps
- * calls: each following call of either entry point records
- * BS_PROFILE_PHASES + 1 HIP events on its stream, until max_steps calls are
- * recorded. For bs_mixed_state_step the phases are attention over all
- * layers, decode row reductions, selection; for bs_lm_head_decode they are
- * the masked-row list, the output-head GEMM with its on-the-fly reduction,
- * and the merge plus selection. bs_profile_end waits for the recorded events
+ * Phase timing of bs_mixed_state_step, bs_lm_head_decode and
+ * bs_dual_cache_refresh (a trace facility; no method content).
+ * bs_profile_begin arms a ring of max_steps calls: each following call of
+ * these entry points records BS_PROFILE_PHASES + 1 HIP events on its stream,
+ * until max_steps calls are recorded. For bs_mixed_state_step the phases are
+ * attention over all layers, decode row reductions, selection; for
+ * bs_lm_head_decode they are the masked-row list, the output-head GEMM with
+ * its on-the-fly reduction, and the merge plus selection; for
+ * bs_dual_cache_refresh the rotated-key and value scatter, the attention,
+ * and an empty third phase. bs_profile_end waits for the recorded events
  * and writes phase_ms[k][ph] (k < *n_steps, ph < BS_PROFILE_PHASES) for up to
  * max_steps calls, then disarms. Events are created once and reused.
  */

@@ -54,7 +54,7 @@ from .gather import gather_active_blocks, scatter_active_blocks
 from .attention import dual_cache_block_attention, attention_rows
 from .decode import parallel_decode, row_stats
 from .lm_head import lm_head_logits, lm_head_decode
-from .refresh import rope, row_positions, dual_cache_refresh
+from .refresh import rope, row_positions, refresh_row, dual_cache_refresh
 from .compact import kv_scatter_compact
 from .step import mixed_state_step
 from . import schedule
@@ -64,6 +64,7 @@ __all__ = [
     "geometry", "validate_reqs", "bbox_cost", "position_ids", "transfer_schedule",
     "effective_compute_ratio", "widen", "gather_active_blocks", "scatter_active_blocks",
     "dual_cache_block_attention", "attention_rows", "parallel_decode", "row_stats",
-    "lm_head_logits", "lm_head_decode", "rope", "row_positions", "dual_cache_refresh",
+    "lm_head_logits", "lm_head_decode", "rope", "row_positions", "refresh_row",
+    "dual_cache_refresh",
     "kv_scatter_compact", "mixed_state_step",
 ]

@@ -31,7 +31,7 @@ import math
 import numpy as np
 
 from .attention import attention_rows
-from .geometry import geometry, position_ids, widen
+from .geometry import position_ids, widen
 
 
 def rope(x, pos, base: float) -> np.ndarray:
@@ -60,6 +60,32 @@ def row_positions(req, W: int) -> np.ndarray:
     return position_ids(mask)[off:off + ln]
 
 
+def refresh_row(req, q_row, k_row, v_row, *, dtype: str = "bf16", rope_base: float = 10000.0,
+                scale: float | None = None, heads=None):
+    """The refresh of one request from its dense row of projections: q_row
+    [W][Hq][D], k_row/v_row [W][Hkv][D] (fp32 values or bf16 bit patterns).
+
+    Returns (out [len][Hq][D] fp64, NaN for heads not computed; K [len][Hkv][D]
+    the rotated keys; V [len][Hkv][D] the values), len = p + g, position t of
+    each array being the request's logical position t (row cell off + t)."""
+    W, Hq, D = q_row.shape
+    Hkv = k_row.shape[1]
+    assert Hq % Hkv == 0
+    G = Hq // Hkv
+    if scale is None or scale <= 0:
+        scale = 1.0 / math.sqrt(D)
+    off, ln = int(req["off"]), int(req["p"]) + int(req["g"])
+    pos = row_positions(req, W)
+    kr = rope(widen(k_row[off:off + ln], dtype), pos[:, None], rope_base)   # [len][Hkv][D]
+    vv = widen(v_row[off:off + ln], dtype)
+    qr = rope(widen(q_row[off:off + ln], dtype), pos[:, None], rope_base)   # [len][Hq][D]
+    out = np.full((ln, Hq, D), np.nan)
+    for h in (range(Hq) if heads is None else heads):
+        c = h // G
+        out[:, h] = attention_rows(qr[:, h], kr[:, c], vv[:, c], scale)
+    return out, kr, vv
+
+
 def dual_cache_refresh(reqs, q, k, v, k_cache, v_cache, *, dtype: str = "bf16",
                        rope_base: float = 10000.0, scale: float | None = None,
                        only=None, heads=None):
@@ -83,26 +109,17 @@ def dual_cache_refresh(reqs, q, k, v, k_cache, v_cache, *, dtype: str = "bf16",
     """
     R, W, Hq, D = q.shape
     Hkv = k.shape[2]
-    assert Hq % Hkv == 0
-    G = Hq // Hkv
-    if scale is None or scale <= 0:
-        scale = 1.0 / math.sqrt(D)
     out = np.full((R, W, Hq, D), np.nan)
     kc = widen(k_cache, dtype).copy()
     vc = widen(v_cache, dtype).copy()
     todo = range(len(reqs)) if only is None else only
-    hs = range(Hq) if heads is None else heads
     for i in todo:
         r = reqs[i]
         row, off, ln = int(r["row"]), int(r["off"]), int(r["p"]) + int(r["g"])
-        pos = row_positions(r, W)
-        kr = rope(widen(k[row, off:off + ln], dtype), pos[:, None], rope_base)   # [len][Hkv][D]
-        vv = widen(v[row, off:off + ln], dtype)
-        qr = rope(widen(q[row, off:off + ln], dtype), pos[:, None], rope_base)   # [len][Hq][D]
+        o, kr, vv = refresh_row(r, q[row], k[row], v[row], dtype=dtype, rope_base=rope_base, scale=scale,
+                                heads=heads)
+        out[row, off:off + ln] = o
         for c in range(Hkv):
             kc[row, c, off:off + ln] = kr[:, c]
             vc[row, c, off:off + ln] = vv[:, c]
-        for h in hs:
-            c = h // G
-            out[row, off:off + ln, h] = attention_rows(qr[:, h], kr[:, c], vv[:, c], scale)
     return out, kc, vc

@@ -26,7 +26,9 @@ __all__ = [
     "bs_sched_counts", "bs_sched_last_error", "Scheduler",
     "bs_attention_workspace_bytes",
     "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
-    "bs_kv_scatter_compact",
+    "bs_kv_scatter_compact", "bs_lm_head_workspace_bytes", "bs_lm_head_decode", "bs_lm_head_pack_bytes",
+    "bs_lm_head_pack", "bs_dual_cache_refresh",
+    "PROFILE_PHASES", "LM_PROFILE_PHASES", "REFRESH_PROFILE_PHASES",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libblockserve.so")
@@ -101,6 +103,8 @@ _SIGS = {
                                  _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "bs_lm_head_pack_bytes": (_sz, [_i32, _i32]),
     "bs_lm_head_pack": (_i32, [_vp, _vp, _i64, _i32, _i32, _i32, _vp, _sz, _vp]),
+    "bs_dual_cache_refresh": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _f32, _vp, _vp, _vp,
+                                     _i32, _i32, _vp, _vp, _vp, _vp]),
     "bs_kv_scatter_compact": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp,
                                      _vp, _i64, _i32, _i32, _vp, _vp, _i64, _i32, _i32, _vp]),
 }
@@ -296,6 +300,14 @@ def bs_lm_head_pack(ctx, w_vocab, w_row_stride, V, d, dt, w_packed, packed_bytes
                                       int(packed_bytes), _stream(stream)), ctx)
 
 
+def bs_dual_cache_refresh(ctx, reqs, L, Hq, Hkv, D, dt, scale, rope_base, q, k, v, R, W, k_cache, v_cache,
+                          out, stream=None):
+    r = _host(reqs, REQ_DTYPE)
+    return _check(lib.bs_dual_cache_refresh(
+        _ptr(ctx), _ptr(r), len(r), L, Hq, Hkv, D, dt, float(scale), float(rope_base), _ptr(q), _ptr(k), _ptr(v),
+        R, W, _ptr(k_cache), _ptr(v_cache), _ptr(out), _stream(stream)), ctx)
+
+
 def bs_kv_scatter_compact(ctx, segs, n_layers, Hkv, D, dt, src_k, src_v, src_layer_stride, R_src, W_src,
                           stg_k, stg_v, stg_layer_stride, R_stg, W_stg, dst_k, dst_v, dst_layer_stride,
                           R_dst, W_dst, stream=None):
@@ -324,6 +336,7 @@ def bs_mixed_state_step(ctx, reqs, L, R, W, layers, Hq, Hkv, D, dt, scale, write
 
 PROFILE_PHASES = ("attention", "decode_rows", "decode_select")          # bs_mixed_state_step
 LM_PROFILE_PHASES = ("rows", "gemm", "merge_select")                      # bs_lm_head_decode
+REFRESH_PROFILE_PHASES = ("rope_kv", "attention", "none")                 # bs_dual_cache_refresh
 
 
 def bs_profile_begin(ctx, max_steps: int) -> None:

@@ -3,6 +3,7 @@
 // descriptor upload through a content-addressed ring of pinned/device slots,
 // and kernel launches on the caller's stream.
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -10,6 +11,7 @@
 #include <vector>
 
 #include "bs_internal.h"
+#include "bs_refresh.h"
 
 using namespace bs;
 
@@ -295,6 +297,46 @@ AttnArgs attention_args(const Slot* sl, int L, int Hq, int Hkv, int D, int R, in
   a.scale_log2e = a.scale * 1.4426950408889634f;
   a.write_back = write_back ? 1 : 0;
   return a;
+}
+
+// ---- refresh work list
+// One item per (request, query head, 256-query chunk). Items that read the
+// same K/V (one request and KV head) stay together on one XCD, so their tiles
+// are shared through that XCD's L2: groups, heaviest first, go to the XCD with
+// the least work so far, and XCD x's queue fills grid slots x, x + 8, ...
+// (workgroup b runs on XCD b % 8); missing slots are empty items.
+void refresh_blob(Blob& blob, const bs_req_desc* reqs, int n, int Hq, int Hkv) {
+  blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
+  const int G = Hq / Hkv;
+  struct Group {
+    int64_t work;
+    int i, c;
+  };
+  std::vector<Group> groups;
+  groups.reserve((size_t)n * Hkv);
+  for (int i = 0; i < n; ++i) {
+    const int64_t len = (int64_t)reqs[i].p + reqs[i].g;
+    for (int c = 0; c < Hkv; ++c) groups.push_back(Group{len * len * G, i, c});
+  }
+  std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.work > y.work; });
+  constexpr int kXcd = 8;
+  std::vector<RefItem> q[kXcd];
+  int64_t load[kXcd] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (const Group& gr : groups) {
+    const int x = (int)(std::min_element(load, load + kXcd) - load);
+    load[x] += gr.work;
+    const bs_req_desc& r = reqs[gr.i];
+    const int len = r.p + r.g;
+    for (int h = gr.c * G; h < (gr.c + 1) * G; ++h)
+      for (int q0 = 0; q0 < len; q0 += kRefQ) q[x].push_back(RefItem{r.row, r.off, len, h, q0, 0, 0, 0});
+  }
+  size_t depth = 0;
+  for (int x = 0; x < kXcd; ++x) depth = std::max(depth, q[x].size());
+  std::vector<RefItem> items(depth * kXcd, RefItem{-1, 0, 0, 0, 0, 0, 0, 0});
+  for (int x = 0; x < kXcd; ++x)
+    for (size_t k = 0; k < q[x].size(); ++k) items[x + k * kXcd] = q[x][k];
+  blob.meta[1] = (int)blob.add(items.data(), sizeof(RefItem) * items.size());
+  blob.meta[2] = (int)items.size();
 }
 
 // ---- decode helpers shared by the K3 entry point and the fused step
@@ -642,6 +684,60 @@ int bs_lm_head_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int d, i
   if (e == hipSuccess) e = prof_mark(c, 3, s);
   if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;
   return finish(c, sl, s, e, "output-head decode launch");
+}
+
+// ------------------------------------------------------------------ dual-cache refresh
+int bs_dual_cache_refresh(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D, bs_dtype dt,
+                          float scale, float rope_base, const void* q, const void* k, const void* v, int R, int W,
+                          void* k_cache, void* v_cache, void* out, void* stream) {
+  if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
+  int st = check_reqs(c, reqs, n, L, R, W);
+  if (st) return st;
+  if (dt != BS_BF16) return fail(c, BS_ERR_UNSUPPORTED, "the refresh runs in bf16 only (dt=%d)", (int)dt);
+  if (Hq < 1 || Hkv < 1) return fail(c, BS_ERR_INVALID_ARG, "Hq, Hkv must be >= 1");
+  if (Hq % Hkv) return fail(c, BS_ERR_UNSUPPORTED, "Hq=%d not a multiple of Hkv=%d", Hq, Hkv);
+  if (D != 128) return fail(c, BS_ERR_UNSUPPORTED, "the refresh needs D = 128 (D=%d)", D);
+  if (!(rope_base == rope_base)) return fail(c, BS_ERR_INVALID_ARG, "rope_base is NaN");
+  if ((int64_t)R * W * Hq > INT32_MAX) return fail(c, BS_ERR_UNSUPPORTED, "R * W * Hq exceeds 2^31");
+  if (n == 0) return BS_OK;
+  if (!q || !k || !v || !k_cache || !v_cache || !out) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+      !aligned(out, 16))
+    return fail(c, BS_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  st = upload(c, s, Key('F', {n, Hq, Hkv}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { refresh_blob(blob, reqs, n, Hq, Hkv); }, &sl);
+  if (st) return st;
+  int max_len = 0;
+  for (int i = 0; i < n; ++i) max_len = std::max(max_len, reqs[i].p + reqs[i].g);
+  const char* base = static_cast<const char*>(sl->d);
+  const bool rope = rope_base > 0.0f;
+  const float nl2b = rope ? (float)(-2.0 * std::log2((double)rope_base) / D) : 0.0f;
+  RefKvArgs kv{};
+  kv.reqs = reinterpret_cast<const bs_req_desc*>(base + sl->meta[0]);
+  kv.Hkv = Hkv; kv.W = W; kv.nl2b = nl2b; kv.rope = rope ? 1 : 0;
+  kv.k = static_cast<const uint16_t*>(k); kv.v = static_cast<const uint16_t*>(v);
+  kv.k_cache = static_cast<uint16_t*>(k_cache); kv.v_cache = static_cast<uint16_t*>(v_cache);
+  RefArgs a{};
+  a.items = reinterpret_cast<const RefItem*>(base + sl->meta[1]);
+  a.Hq = Hq; a.Hkv = Hkv; a.G = Hq / Hkv; a.W = W;
+  const float sc = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
+  a.scale_log2e = sc * 1.4426950408889634f;
+  a.nl2b = nl2b; a.rope = kv.rope;
+  a.q = static_cast<const uint16_t*>(q); a.out = static_cast<uint16_t*>(out);
+  a.k_cache = kv.k_cache; a.v_cache = kv.v_cache;
+  // phase events (when the ring is armed): rotated keys and values | attention
+  hipError_t e = prof_mark(c, 0, s);
+  if (e == hipSuccess) e = launch_refresh_kv(kv, n, max_len, s);
+  if (e == hipSuccess) e = prof_mark(c, 1, s);
+  if (e == hipSuccess) e = launch_refresh_attn(a, sl->meta[2], s);
+  if (e == hipSuccess) e = prof_mark(c, 2, s);
+  if (e == hipSuccess) e = prof_mark(c, 3, s);
+  if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;
+  return finish(c, sl, s, e, "refresh launch");
 }
 
 // ------------------------------------------------------------------ fused step

@@ -71,6 +71,8 @@ def test_calls_without_context_fail_before_any_device_work():
     assert bs.lib.bs_lm_head_decode(null, None, 0, 8, 64, 10, 0, None, None, None, None, 0.9, 1, -1, None,
                                     None, None, None, None, 0, None) == 1
     assert bs.lib.bs_lm_head_pack(null, None, 64, 10, 64, 0, None, 0, None) == 1
+    assert bs.lib.bs_dual_cache_refresh(null, None, 0, 32, 4, 2, 128, 1, 0.0, 1e4, None, None, None, 1, 1,
+                                        None, None, None, None) == 1
     assert "ctx is NULL" in bs.bs_last_error()
 
 

@@ -126,18 +126,18 @@ MUTANTS = [
      [(TR.test_rope_pairs_feature_f_with_f_plus_half,), (TR.test_rope_equals_complex_multiplication,)]),
     (RFR, "return position_ids(mask)[off:off + ln]", "return np.arange(off, off + ln)", "dual_cache_refresh",
      [(TR.test_placement_in_the_box_does_not_matter,)]),
-    (RFR, "qr = rope(widen(q[row, off:off + ln], dtype), pos[:, None], rope_base)",
-     "qr = widen(q[row, off:off + ln], dtype)", "dual_cache_refresh",
+    (RFR, "qr = rope(widen(q_row[off:off + ln], dtype), pos[:, None], rope_base)",
+     "qr = widen(q_row[off:off + ln], dtype)", "dual_cache_refresh",
      [(TR.test_block_rows_match_block_attention_on_the_refreshed_cache,)]),
-    (RFR, "vv = widen(v[row, off:off + ln], dtype)",
-     "vv = rope(widen(v[row, off:off + ln], dtype), pos[:, None], rope_base)", "dual_cache_refresh",
+    (RFR, "vv = widen(v_row[off:off + ln], dtype)",
+     "vv = rope(widen(v_row[off:off + ln], dtype), pos[:, None], rope_base)", "dual_cache_refresh",
      [(TR.test_uniform_values_and_one_token_row,)]),
     (RFR, "kc[row, c, off:off + ln] = kr[:, c]", "kc[row, c, off:off + ln] = widen(k[row, off:off + ln, c], dtype)",
      "dual_cache_refresh", [(TR.test_block_rows_match_block_attention_on_the_refreshed_cache,)]),
     (RFR, "c = h // G", "c = h % Hkv", "dual_cache_refresh", [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
     (RFR, "scale = 1.0 / math.sqrt(D)", "scale = 1.0 / D", "dual_cache_refresh",
      [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
-    (RFR, "kr = rope(widen(k[row, off:off + ln], dtype)", "kr = rope(widen(k[row, off + 1:off + ln + 1], dtype)",
+    (RFR, "kr = rope(widen(k_row[off:off + ln], dtype)", "kr = rope(widen(k_row[off + 1:off + ln + 1], dtype)",
      "dual_cache_refresh", [(TR.test_unrotated_refresh_matches_torch_sdpa, "f32")]),
 ]
 

@@ -7,7 +7,7 @@
 
 namespace bs {
 
-constexpr int kRefQ = 256;     // query positions per workgroup (4 waves x 64)
+constexpr int kRefQ = 256;     // query positions per workgroup (8 waves x 32)
 constexpr int kRefKT = 64;     // keys per LDS stage
 constexpr int kRefNS = 4;      // LDS stages (4 x 32 KiB of K and V)
 

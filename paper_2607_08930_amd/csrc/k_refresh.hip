@@ -12,10 +12,9 @@
 //                from the token-major projections into the head-major cache.
 //                HBM-bound: every byte is read once and written once.
 // k_refresh_attn full-row attention over the refreshed cache, the queries
-//                rotated as they are loaded. MFMA-bound: a workgroup of four
-//                waves owns 256 query positions of one head, one wave per SIMD
-//                and 64 queries per wave, so every K and V fragment read from
-//                LDS feeds two 32x32x16 MFMAs. K/V tiles of 64 keys stream
+//                rotated as they are loaded. A workgroup of eight waves owns
+//                256 query positions of one head, two waves per SIMD and 32
+//                queries per wave (32x32x16 MFMAs). K/V tiles of 64 keys stream
 //                HBM/L2 -> LDS by direct DMA through a 4-stage ring, two tiles
 //                in flight. Inside a wave the loop is software-pipelined by
 //                32-key sub-tiles: while the exponentials of sub-tile u run on
@@ -40,8 +39,14 @@ __device__ inline uint32_t pack_bf16(float lo, float hi) {
 }
 
 // Rotate the feature pairs (x1[e], x2[e]) of 8 consecutive features f0 .. f0+7
-// of the first half (partners f + D/2 in x2) by pos * exp2(f * nl2b).
+// of the first half (partners f + D/2 in x2) by the angle pos * exp2(f * nl2b).
+// The angle is formed in turns, pos * exp2(f * nl2b - log2(2 pi)); its
+// fractional part (exact) feeds the hardware sine and cosine, which take
+// turns. The fp32 roundings of the inverse frequency and of the product leave
+// an angle error of a few 2^-23 relative, under 4e-4 rad for positions below
+// 2048.
 __device__ inline void rope8(v4u& x1, v4u& x2, int f0, float pos, float nl2b) {
+  constexpr float kNegLog2TwoPi = -2.6514961294723187f;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     float a[2], b[2];
@@ -50,9 +55,9 @@ __device__ inline void rope8(v4u& x1, v4u& x2, int f0, float pos, float nl2b) {
     float ya[2], yb[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const float ang = pos * exp2f((float)(f0 + 2 * w + e) * nl2b);
-      float sn, cs;
-      sincosf(ang, &sn, &cs);
+      const float turns = pos * __builtin_amdgcn_exp2f(fmaf((float)(f0 + 2 * w + e), nl2b, kNegLog2TwoPi));
+      const float fr = __builtin_amdgcn_fractf(turns);
+      const float sn = __builtin_amdgcn_sinf(fr), cs = __builtin_amdgcn_cosf(fr);
       ya[e] = a[e] * cs - b[e] * sn;
       yb[e] = b[e] * cs + a[e] * sn;
     }
@@ -101,15 +106,23 @@ __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
   return lsum;
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
+// NW waves of QW 32-query blocks each (NW * QW * 32 = 256 queries per
+// workgroup) share the K/V ring. QW = 2 feeds every LDS fragment to two
+// MFMAs but needs about 400 registers (one wave per SIMD, so nothing hides
+// the softmax arithmetic and the LDS latency: 20% slower on the Dream-7B
+// shape); QW = 1 reads twice the LDS bytes per MFMA and fits two waves per
+// SIMD (209 VGPRs), which is what the launch uses.
+template <int D, int QW, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
   static_assert(D == 128, "the refresh attention is laid out for D = 128");
+  static_assert(NW * QW * 32 == kRefQ, "a workgroup covers kRefQ queries");
   constexpr int KT = kRefKT, NS = kRefNS;
   constexpr int NKK = D / 16;        // K-steps of a score MFMA
   constexpr int NDT = D / 32;        // 32-feature output tiles
   constexpr int TILE = KT * D;       // elements of one K (or V) tile
   constexpr int STAGE = 2 * TILE;    // K tile, then V tile
-  constexpr int PB = 8;              // 1 KiB DMA blocks per stage and wave (32 / 4 waves)
+  constexpr int PB = 32 / NW;        // 1 KiB DMA blocks per stage and wave (32 per stage)
+  constexpr int WPT = NW / 2;        // waves per tensor (K, then V)
   __shared__ __align__(1024) uint16_t ring[NS * STAGE];
 
   const RefItem it = a.items[blockIdx.x];
@@ -118,17 +131,18 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
   const int lane = threadIdx.x & 63, g = lane >> 5, n = lane & 31;
   const int len = it.len, h = it.h, c = h / a.G;
   const int ntiles = (len + KT - 1) / KT, nsub = (len + 31) / 32;
-  const int qbase = it.q0 + 64 * w;                  // first query of this wave
+  const int qbase = it.q0 + 32 * QW * w;             // first query of this wave
   const bool active = qbase < len;                   // wave-uniform
 
   const int64_t cache_off = (((int64_t)it.row * a.Hkv + c) * a.W + it.off) * D;
   const uint16_t* kcb = a.k_cache + cache_off;
   const uint16_t* vcb = a.v_cache + cache_off;
 
-  // DMA: wave w moves blocks 8w .. 8w + 7 of a stage; waves 0-1 the K tile,
-  // 2-3 the V tile. Block b covers tile rows 4 (b % 16) .. + 3; lane l fills
-  // row 4 (b % 16) + l / 16, slot l % 16, from global chunk slot ^ swz(row).
-  const int tensor = w >> 1;
+  // DMA: wave w moves PB blocks of a stage; the first NW/2 waves the K tile,
+  // the others the V tile. Block rb of a tile covers its rows 4 rb .. + 3;
+  // lane l fills row 4 rb + l / 16, slot l % 16, from global chunk
+  // slot ^ swz(row).
+  const int tensor = w / WPT;
   const uint16_t* tb_src = tensor ? vcb : kcb;
   const uint32_t ring_lds = lds_addr(ring);
   auto issue = [&](int tile) {
@@ -138,7 +152,7 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
       const uint64_t base = uniform64(tb_src + (int64_t)t0 * D);
 #pragma unroll
       for (int k = 0; k < PB; ++k) {
-        const int rb = (w & 1) * PB + k;
+        const int rb = (w % WPT) * PB + k;
         const int row = rb * 4 + (lane >> 4);
         const int chunk = (lane & 15) ^ swz16(row);
         dma16_sv(sbase + (uint32_t)((tensor * TILE + rb * 4 * D) * 2), base, (uint32_t)(row * D + chunk * 8) * 2u);
@@ -147,7 +161,7 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
       // ragged last tile: rows past the row end repeat its last key (masked)
 #pragma unroll
       for (int k = 0; k < PB; ++k) {
-        const int rb = (w & 1) * PB + k;
+        const int rb = (w % WPT) * PB + k;
         const int row = rb * 4 + (lane >> 4);
         const int chunk = (lane & 15) ^ swz16(row);
         const int t = min(t0 + row, len - 1);
@@ -161,12 +175,12 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
   if (ntiles > 1) issue(1);
   if (ntiles > 2) issue(2);
 
-  // queries of this lane's column n of query blocks 0 and 1, rotated, as MFMA
-  // B operands: feature 16 kk + 8 g + e; the rotation partner of kk < NKK/2
-  // is chunk kk + NKK/2 of the same lane
-  bf16x8_t qb[2][NKK];
+  // queries of this lane's column n of each query block, rotated, as MFMA B
+  // operands: feature 16 kk + 8 g + e; the rotation partner of kk < NKK/2 is
+  // chunk kk + NKK/2 of the same lane
+  bf16x8_t qb[QW][NKK];
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < QW; ++b) {
     const int j = min(qbase + 32 * b + n, len - 1);
     const uint16_t* qp = a.q + (((int64_t)it.row * a.W + it.off + j) * a.Hq + h) * D;
     v4u x[NKK];
@@ -198,43 +212,36 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
         voff[dt][ks][h2] = row * D + (((col >> 3) ^ swz16(row)) * 8) + (col & 7);
       }
 
-  f32x16_t o[2][NDT];
+  f32x16_t o[QW][NDT];
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+  for (int b = 0; b < QW; ++b)
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) o[b][dt][rr] = 0.0f;
-  float mrun[2] = {-__builtin_inff(), -__builtin_inff()}, lsum[2] = {0.0f, 0.0f};
+  float mrun[QW], lsum[QW], alpha_pend[QW];
+#pragma unroll
+  for (int b = 0; b < QW; ++b) {
+    mrun[b] = -__builtin_inff();
+    lsum[b] = 0.0f;
+    alpha_pend[b] = 1.0f;
+  }
+  bool resc_pend = false;
 
   // K rows of sub-tile u (32 keys) start at element sub_k(u); its V rows at + TILE
   auto sub_k = [&](int u) { return ((u >> 1) % NS) * STAGE + (u & 1) * 32 * D; };
-  auto scores = [&](int u, f32x16_t& s0, f32x16_t& s1) {
-    const uint16_t* kt = ring + sub_k(u);
-#pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      s0[rr] = 0.0f;
-      s1[rr] = 0.0f;
-    }
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kt + koff[kk]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qb[0][kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qb[1][kk], s1, 0, 0, 0);
-    }
+  auto vfrag = [&](const uint16_t* vs, int dt, int ks) {
+    const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
+    const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
+    return (bf16x8_t)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  auto pv = [&](int u, const bf16x8_t (&p)[2][2]) {
-    const uint16_t* vs = ring + sub_k(u) + TILE;
+  auto rescale = [&]() {
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
+    for (int b = 0; b < QW; ++b)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
-        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
-        const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p[0][ks], o[0][dt], 0, 0, 0);
-        o[1][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p[1][ks], o[1][dt], 0, 0, 0);
-      }
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) o[b][dt][rr] *= alpha_pend[b];
   };
 
   // tile 0 landed (tiles 1, 2 may still be in flight), visible to all waves
@@ -246,15 +253,26 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
     wait_vm_c<0>();
   __syncthreads();
 
-  f32x16_t sc[2], sn[2];
-  bf16x8_t pprev[2][2], pcur[2][2];
+  f32x16_t sc[QW], sn[QW];
+  bf16x8_t pprev[QW][2], pcur[QW][2];
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+  for (int b = 0; b < QW; ++b)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pprev[b][ks][e] = (__bf16)0.0f;
-  if (active) scores(0, sc[0], sc[1]);
+  if (active) {
+#pragma unroll
+    for (int b = 0; b < QW; ++b)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) sc[b][rr] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(ring + koff[kk]);
+#pragma unroll
+      for (int b = 0; b < QW; ++b) sc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qb[b][kk], sc[b], 0, 0, 0);
+    }
+  }
 
   for (int u = 0; u < nsub; ++u) {
     const int un = u + 1;
@@ -270,39 +288,56 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
       if (T + 2 < ntiles) issue(T + 2);
     }
     if (!active) continue;
+    // a reference max raised in the previous iteration rescales the
+    // accumulators now, after P V of its predecessor and before its own (at
+    // the top of the body, so the loop's tail stays one basic block in which
+    // the exponentials and the MFMAs can interleave)
+    if (resc_pend) {
+      rescale();
+      resc_pend = false;
+    }
+    // K fragments of sub-tile u + 1 (on the last iteration a resident one
+    // again, its scores discarded), issued first so their latency hides under
+    // the softmax arithmetic; V of u - 1 (of sub-tile 0 on the first
+    // iteration, with zero weights)
+    const uint16_t* kt = ring + sub_k(un < nsub ? un : u);
+    const uint16_t* vs = ring + sub_k(u > 0 ? u - 1 : 0) + TILE;
+    bf16x8_t kf[NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) kf[kk] = *reinterpret_cast<const bf16x8_t*>(kt + koff[kk]);
     const int k0 = u * 32;
     if (k0 + 32 > len) {                               // ragged last sub-tile
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
         const int key = k0 + 8 * (rr >> 2) + 4 * g + (rr & 3);
         if (key >= len) {
-          sc[0][rr] = -__builtin_inff();
-          sc[1][rr] = -__builtin_inff();
+#pragma unroll
+          for (int b = 0; b < QW; ++b) sc[b][rr] = -__builtin_inff();
         }
       }
     }
-    // running max per query (log2 units); lazy rescale by at most 2^8
-    float alpha[2] = {1.0f, 1.0f};
-    bool resc[2];
+    // running max per query (log2 units), lazily raised: the reference max
+    // moves only when a score exceeds it by 2^8, so the accumulators are
+    // rescaled a handful of times per row (alpha = 1 when it stays)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      float mx = sc[b][0];
+    for (int b = 0; b < QW; ++b) {
+      float mx = vmax(sc[b][0], sc[b][1]);
 #pragma unroll
-      for (int rr = 1; rr < 16; ++rr) mx = vmax(mx, sc[b][rr]);
-      mx = vmax(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;
-      resc[b] = __builtin_amdgcn_ballot_w64(mx > mrun[b] + 8.0f) != 0;
-      if (resc[b]) {
-        const float mnew = fmaxf(mrun[b], mx);
-        alpha[b] = __builtin_amdgcn_exp2f(mrun[b] - mnew);
-        lsum[b] *= alpha[b];
-        mrun[b] = mnew;
-      }
+      for (int rr = 2; rr < 16; ++rr) mx = vmax(mx, sc[b][rr]);
+      // the other half-wave holds the other 16 keys of this query
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = vmax(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * a.scale_log2e;
+      const bool resc = __builtin_amdgcn_ballot_w64(mx > mrun[b] + 8.0f) != 0;
+      const float mnew = resc ? fmaxf(mrun[b], mx) : mrun[b];
+      alpha_pend[b] = __builtin_amdgcn_exp2f(mrun[b] - mnew);
+      lsum[b] *= alpha_pend[b];
+      mrun[b] = mnew;
+      resc_pend |= resc;
     }
-    // probabilities of sub-tile u (VALU) beside the scores of u + 1 and P V of
-    // u - 1 (matrix core); the last iteration re-reads a resident sub-tile
-    // and discards the scores
+    // probabilities of sub-tile u on the VALU, interleaved with the matrix
+    // core's scores of u + 1 and P V of u - 1
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < QW; ++b) {
       const float nm = -mrun[b];
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
@@ -311,30 +346,56 @@ __global__ __launch_bounds__(256, 1) void k_refresh_attn(RefArgs a) {
       }
       lsum[b] = add_weights(add_weights(lsum[b], pcur[b][0]), pcur[b][1]);
     }
-    scores(un < nsub ? un : u, sn[0], sn[1]);
-    pv(u > 0 ? u - 1 : 0, pprev);
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-      if (resc[b]) {
+    for (int b = 0; b < QW; ++b)
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
+      for (int rr = 0; rr < 16; ++rr) sn[b][rr] = 0.0f;
 #pragma unroll
-          for (int rr = 0; rr < 16; ++rr) o[b][dt][rr] *= alpha[b];
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+      for (int b = 0; b < QW; ++b) sn[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qb[b][kk], sn[b], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8_t va = vfrag(vs, dt, ks);
+#pragma unroll
+        for (int b = 0; b < QW; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pprev[b][ks], o[b][dt], 0, 0, 0);
       }
+    // schedule: the max/rescale arithmetic, then one MFMA per few VALU ops
+    __builtin_amdgcn_sched_group_barrier(0x002, 20 * QW, 0);
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int i = 0; i < 16 * QW; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+#pragma unroll
+    for (int b = 0; b < QW; ++b) {
       sc[b] = sn[b];
       pprev[b][0] = pcur[b][0];
       pprev[b][1] = pcur[b][1];
     }
   }
   if (!active) return;
-  pv(nsub - 1, pprev);
+  if (resc_pend) rescale();
+  {
+    const uint16_t* vs = ring + sub_k(nsub - 1) + TILE;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8_t va = vfrag(vs, dt, ks);
+#pragma unroll
+        for (int b = 0; b < QW; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pprev[b][ks], o[b][dt], 0, 0, 0);
+      }
+  }
 
   // lane (g, n): O^T[feature 32 dt + 8 (rr / 4) + 4 g + rr % 4][query n of block b]
   typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < QW; ++b) {
     const int j = qbase + 32 * b + n;
     const float lt = lsum[b] + __shfl_xor(lsum[b], 32, 64);
     if (j < len) {
@@ -363,7 +424,8 @@ hipError_t launch_refresh_kv(const RefKvArgs& a, int n, int max_len, hipStream_t
 }
 
 hipError_t launch_refresh_attn(const RefArgs& a, int n_items, hipStream_t s) {
-  hipLaunchKernelGGL(k_refresh_attn<128>, dim3((unsigned)n_items), dim3(256), 0, s, a);
+  constexpr int QW = 1, NW = kRefQ / (32 * QW);
+  hipLaunchKernelGGL((k_refresh_attn<128, QW, NW>), dim3((unsigned)n_items), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 

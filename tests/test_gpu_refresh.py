@@ -9,7 +9,8 @@ Tolerances. Attention: the bf16 bound of the block attention (max abs error
 1e-2 and max|d| / max|O| <= 1e-2). Cached keys: the kernel rounds the rotated
 fp32 value to bf16 (half an ulp: at most 2^-8 of the value, 8 significant
 bits) after computing the angle in fp32 (position times an fp32 inverse
-frequency: under 4e-4 rad for positions below 2048), so |K_gpu - K_ref| <=
+frequency, in turns, through the hardware sine and cosine: under 4e-4 rad for
+positions below 2048), so |K_gpu - K_ref| <=
 2^-8 |K_ref| + 4e-4 |pair| + 1e-7, |pair|
 being the norm of the feature pair the element belongs to. Values are copied
 and must match bit for bit; with the rotation disabled, so must the keys."""

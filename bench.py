@@ -10,7 +10,10 @@ rather than writes: a written sweep would leave the cache full of dirty lines
 whose write-back would then be charged to the timed step.
 
 The headline (`ms_per_step`, `value`) times K plain steps, each bracketed by
-HIP events on the step's stream. A second region of K steps arms the library's
+HIP events on the step's stream: the start event without a system-scope fence
+(the cache maintenance it would do belongs to the untimed restore), the end
+event with it (the step's own dirty lines are written back inside the
+region). A second region of K steps arms the library's
 event ring, which records the phase times (attention over all layers, decode
 row reductions, selection) on the same stream; the roofline's launch duration
 comes from it. The ring's events cost a few microseconds each, so they are
@@ -122,6 +125,58 @@ def source_hash(kernel):
 
 def traffic_file(workload):
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+
+
+class HipEvent:
+    """A HIP timing event on the process's HIP runtime (the one torch loaded).
+    The start event of a timed region is created with
+    hipEventDisableSystemFence: recording it performs no system-scope cache
+    write-back and invalidation, which would otherwise charge the previous
+    (untimed) work's cache maintenance to the region. The end event keeps the
+    default fence, so the region's own dirty lines are written back inside
+    it."""
+    _lib = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, fence: bool):
+        import ctypes
+        if HipEvent._lib is None:
+            paths = set()
+            with open("/proc/self/maps") as f:
+                for line in f:
+                    p_ = line.split()[-1] if line.strip() else ""
+                    if "libamdhip64" in p_:
+                        paths.add(os.path.realpath(p_))
+            assert len(paths) == 1, f"expected one HIP runtime, found {sorted(paths)}"
+            lib = ctypes.CDLL(paths.pop())
+            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._lib = lib
+        self._ct = __import__("ctypes")
+        self.h = self._ct.c_void_p()
+        st = HipEvent._lib.hipEventCreateWithFlags(self._ct.byref(self.h), 0 if fence else self.DISABLE_SYSTEM_FENCE)
+        assert st == 0, f"hipEventCreateWithFlags failed ({st})"
+
+    def record(self, stream):
+        st = HipEvent._lib.hipEventRecord(self.h, self._ct.c_void_p(stream.cuda_stream))
+        assert st == 0, f"hipEventRecord failed ({st})"
+
+    def elapsed_time(self, end) -> float:
+        ms = self._ct.c_float()
+        st = HipEvent._lib.hipEventElapsedTime(self._ct.byref(ms), self.h, end.h)
+        assert st == 0, f"hipEventElapsedTime failed ({st})"
+        return float(ms.value)
+
+    def __del__(self):
+        if self._lib is not None and self.h:
+            self._lib.hipEventDestroy(self.h)
+
+
+def region_events():
+    """(start, end) events of one timed region (see HipEvent)."""
+    return HipEvent(fence=False), HipEvent(fence=True)
 
 
 def read_traffic(workload, kernel):
@@ -299,7 +354,7 @@ def lm_head_bench(args):
             dt.copy_(t0)
             dm.copy_(m0)
             flush.sum()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = region_events()
             e0.record(stream)
             fn()
             e1.record(stream)
@@ -418,7 +473,7 @@ def refresh_bench(args):
         res = []
         for _ in range(kreps):
             flush.sum()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = region_events()
             e0.record(stream)
             fn()
             e1.record(stream)
@@ -637,7 +692,7 @@ def main():
     def timed(ring):
         """K steps, each bracketed by HIP events on the step's stream; with
         ring, the library's phase events are recorded inside every step."""
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        evs = [region_events() for _ in range(args.steps)]
         if ring:
             bs.bs_profile_begin(ctx, args.steps)
         torch.cuda.synchronize()

@@ -341,7 +341,9 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
  * bs_dual_cache_refresh the rotated-key and value scatter, the attention,
  * and an empty third phase. bs_profile_end waits for the recorded events
  * and writes phase_ms[k][ph] (k < *n_steps, ph < BS_PROFILE_PHASES) for up to
- * max_steps calls, then disarms. Events are created once and reused.
+ * max_steps calls, then disarms. Events are created once and reused; they
+ * are timing-only events (hipEventDisableSystemFence), so a mark adds no
+ * cache write-back or invalidation between the phases.
  */
 #define BS_PROFILE_PHASES 3
 int bs_profile_begin(bs_ctx* ctx, int max_steps);

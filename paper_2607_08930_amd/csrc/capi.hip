@@ -804,8 +804,10 @@ int bs_profile_begin(bs_ctx* c, int max_steps) {
   Prof& p = c->prof;
   const size_t need = (size_t)max_steps * (kProfPhases + 1);
   while (p.ev.size() < need) {
+    // timing-only events: no system-scope fence (cache write-back and
+    // invalidate) at each mark, which would otherwise be charged to the phases
     hipEvent_t e = nullptr;
-    hipError_t r = hipEventCreate(&e);
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) return hip_fail(c, r, "hipEventCreate(profile)");
     p.ev.push_back(e);
   }

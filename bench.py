@@ -732,6 +732,22 @@ def main():
                 "algorithmic_bytes_per_launch": logits_bytes, "avg_launch_ms": round(rows_ms, 5)}
     roof["traffic"] = read_traffic(w.name, roof["kernel"])
     ctx.close()
+    # reference: a plain device copy that moves the step's algorithmic bytes
+    # (half read, half written), cold, timed like a step
+    half = (step_bytes // 2 + 255) // 256 * 256
+    csrc = torch.ones(half // 4, dtype=torch.float32, device="cuda")
+    cdst = torch.empty_like(csrc)
+    copy_ms = []
+    for k in range(args.steps):
+        flush.sum()
+        e0, e1 = region_events()
+        e0.record(stream)
+        cdst.copy_(csrc)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        copy_ms.append(e0.elapsed_time(e1))
+    copy_ms = float(np.median(copy_ms))
+    del csrc, cdst
     res = {
         "metric": "denoised block positions/s per mixed-state step",
         "value": round(value, 1), "unit": "positions/s", "n_gpus": 1, "steps": args.steps,
@@ -749,6 +765,9 @@ def main():
         "wall_ms_per_step_incl_restore": round(wall, 5),
         "step_ms_p10_p90": [round(float(np.percentile(step_ms, 10)), 5), round(float(np.percentile(step_ms, 90)), 5)],
         "ms_per_step_with_phase_events": round(float(np.median(ring_ms)), 5),
+        "copy_reference": {"bytes": 2 * half, "ms": round(copy_ms, 5),
+                           "GBps": round(2 * half / (copy_ms / 1e3) / 1e9, 1),
+                           "what": "device copy of the step's byte count (half read, half written), cold"},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

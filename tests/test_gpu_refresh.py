@@ -9,10 +9,11 @@ Tolerances. Attention: the bf16 bound of the block attention (max abs error
 1e-2 and max|d| / max|O| <= 1e-2). Cached keys: the kernel rounds the rotated
 fp32 value to bf16 (half an ulp: at most 2^-8 of the value, 8 significant
 bits) after computing the angle in fp32 (position times an fp32 inverse
-frequency, in turns, through the hardware sine and cosine: under 4e-4 rad for
-positions below 2048), so |K_gpu - K_ref| <=
-2^-8 |K_ref| + 4e-4 |pair| + 1e-7, |pair|
-being the norm of the feature pair the element belongs to. Values are copied
+frequency, in turns, through the hardware sine and cosine: a few 2^-23 of
+the angle, bounded here by 2.5e-7 * pos rad, plus 2e-6 for the hardware sine
+itself), so |K_gpu - K_ref| <= 2^-8 |K_ref| + (2.5e-7 * pos + 2e-6) * |pair|
++ 1e-7, |pair| being the norm of the feature pair the element belongs to and
+pos its position. Values are copied
 and must match bit for bit; with the rotation disabled, so must the keys."""
 import numpy as np
 import pytest
@@ -58,7 +59,8 @@ def check_keys(got_bits, ref, k_bits, label):
     half = x.shape[-1] // 2
     pair = np.sqrt(x[..., :half] ** 2 + x[..., half:] ** 2)
     pair = np.concatenate([pair, pair], axis=-1)
-    bound = 2.0 ** -8 * np.abs(ref) + 4e-4 * pair + 1e-7
+    pos = np.arange(x.shape[0], dtype=np.float64).reshape((-1,) + (1,) * (x.ndim - 1))
+    bound = 2.0 ** -8 * np.abs(ref) + (2.5e-7 * pos + 2e-6) * pair + 1e-7
     bad = np.abs(g - ref) > bound
     assert not bad.any(), f"{label}: {int(bad.sum())} cached keys outside the bound, worst " \
                           f"{float(np.max(np.abs(g - ref) - bound)):.3e}"
@@ -173,6 +175,66 @@ def test_full_size_sampled(ctx, cfg):
         e, mx = check_request(w, i, out_h[row, off:off + ln], dkc_h[row, :, off:off + ln],
                               dvc_h[row, :, off:off + ln], q, k, v, base, heads=heads, label=w.name)
         say(f"  request {i} (len {ln}) heads {heads}: max abs error {e:.2e} of max |O| {mx:.2e}")
+
+
+def test_empty_batch_is_a_no_op(ctx):
+    torch, bs, bstep = lazy()
+    t = torch.full((64,), 3.0, dtype=torch.bfloat16, device="cuda")
+    empty = np.zeros(0, synth.REQ_DTYPE)
+    bs.bs_dual_cache_refresh(ctx, empty, 32, 4, 2, 128, bs.BS_BF16, 0.0, 1e4, t, t, t, 1, 1, t, t, t)
+    torch.cuda.synchronize()
+    assert bool((t == 3.0).all())
+
+
+def test_long_row(ctx):
+    # one row of 4096 positions next to a short one: 16 query chunks, 64 key
+    # tiles, rotation angles up to 4095 rad on the first feature pair
+    torch, bs, bstep = lazy()
+    w = synth.custom(32, 4, 2, 128, 10, "bf16", [3000, 10], [1096, 22], [0, 0], kv_sigma=1 / np.sqrt(128))
+    say(f"refresh long row: lens {[int(r['p'] + r['g']) for r in w.reqs]} W={w.W}")
+    q, k, v = synth.gen_refresh(w)
+    kc, vc = synth.poison_cache(w, *synth.gen_cache(w))
+    out, dkc, dvc = run_refresh(ctx, w, q, k, v, kc, vc, 1e6)
+    out_h, kc_h, vc_h = bstep.to_host(out), bstep.to_host(dkc), bstep.to_host(dvc)
+    for i, heads in ((0, [0, 3]), (1, None)):
+        r = w.reqs[i]
+        row, off, ln = int(r["row"]), int(r["off"]), int(r["p"] + r["g"])
+        e, mx = check_request(w, i, out_h[row, off:off + ln], kc_h[row, :, off:off + ln],
+                              vc_h[row, :, off:off + ln], q, k, v, 1e6, heads=heads, label="long row")
+        say(f"  request {i} (len {ln}): max abs error {e:.2e} of max |O| {mx:.2e}")
+
+
+def test_refresh_then_block_step(ctx):
+    # the block attention of the next denoising step, run on the refreshed
+    # cache with the block's rotated queries and keys (rotated on the host
+    # and rounded to bf16), reproduces the refresh's outputs at the block rows
+    torch, bs, bstep = lazy()
+    w = synth.custom(32, 4, 2, 128, 10, "bf16", [5, 300, 77], [64, 200, 96], [1, 3, 2], kv_sigma=1 / np.sqrt(128))
+    base = 5e5
+    q, k, v = synth.gen_refresh(w)
+    kc, vc = synth.gen_cache(w)
+    out, dkc, dvc = run_refresh(ctx, w, q, k, v, kc, vc, base)
+    out_h = oracle.widen(bstep.to_host(out), "bf16")
+    qb = np.zeros((w.n, w.L, w.Hq, w.D), np.float32)
+    kn = np.zeros((w.n, w.L, w.Hkv, w.D), np.float32)
+    vn = np.zeros_like(kn)
+    for i, (r, (s0, B, ln)) in enumerate(zip(w.reqs, w.spans())):
+        row, off = int(r["row"]), int(r["off"])
+        pos = np.arange(s0, s0 + B)[:, None]
+        qb[i, :B] = oracle.rope(oracle.widen(q[row, off + s0:off + s0 + B], "bf16"), pos, base)
+        kn[i, :B] = oracle.rope(oracle.widen(k[row, off + s0:off + s0 + B], "bf16"), pos, base)
+        vn[i, :B] = oracle.widen(v[row, off + s0:off + s0 + B], "bf16")
+    dq, dkn, dvn = (bstep.to_device(synth.f32_to_bf16_bits(x), "bf16") for x in (qb, kn, vn))
+    blk = torch.full(dq.shape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    bs.bs_dual_cache_block_attention(ctx, w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 0.0, dq, dkn, dvn, dkc, dvc,
+                                     w.R, w.W, 0, blk)
+    torch.cuda.synchronize()
+    got = oracle.widen(bstep.to_host(blk), "bf16")
+    for i, (r, (s0, B, ln)) in enumerate(zip(w.reqs, w.spans())):
+        row, off = int(r["row"]), int(r["off"])
+        ref = out_h[row, off + s0:off + s0 + B]
+        d = np.abs(got[i, :B] - ref).max()
+        assert d <= ATT_TOL["bf16"] and d / np.abs(ref).max() <= 2 * ATT_REL, f"request {i}: {d:.3e}"
 
 
 def test_rejects_unsupported_arguments(ctx):

@@ -269,7 +269,7 @@ int bs_lm_head_pack(bs_ctx* ctx, const void* w_vocab, int64_t w_row_stride, int 
  * requests' logical cells are read (padding may hold NaN) or written (every
  * other cell of out and the caches is left unchanged). q, k, v must not
  * overlap the caches or out. The descriptors are validated as everywhere
- * (L and k only there); R * W * Hq < 2^31.
+ * (L and k only there); R * W * Hq < 2^31; n <= 65535.
  * Supported: dt = BS_BF16, D = 128, Hq % Hkv == 0. All pointers 16-byte
  * aligned. Two launches on `stream` (keys and values, then attention).
  */

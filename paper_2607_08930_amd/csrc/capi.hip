@@ -699,6 +699,7 @@ int bs_dual_cache_refresh(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int 
   if (D != 128) return fail(c, BS_ERR_UNSUPPORTED, "the refresh needs D = 128 (D=%d)", D);
   if (!(rope_base == rope_base)) return fail(c, BS_ERR_INVALID_ARG, "rope_base is NaN");
   if ((int64_t)R * W * Hq > INT32_MAX) return fail(c, BS_ERR_UNSUPPORTED, "R * W * Hq exceeds 2^31");
+  if (n > 65535) return fail(c, BS_ERR_UNSUPPORTED, "n=%d requests exceed the 65535 of one launch", n);
   if (n == 0) return BS_OK;
   if (!q || !k || !v || !k_cache || !v_cache || !out) return fail(c, BS_ERR_INVALID_ARG, "tensor pointer is NULL");
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||

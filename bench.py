@@ -281,6 +281,18 @@ class DeviceProvider:
         n = len(ids)
         return [(q[:n], kn[:n], vn[:n]) for q, kn, vn in self.layers], self.logits[:n]
 
+    def refresh(self, ids, descs, cycle):
+        """Projections of the whole box at a block start, made once and reused."""
+        torch, cfg = self.torch, self.cfg
+        if not hasattr(self, "box"):
+            g, td, s = self.gen, torch.bfloat16, 1.0 / np.sqrt(cfg.D)
+            R, W = cfg.rows, cfg.width
+            self.box = [(torch.randn((R, W, cfg.Hq, cfg.D), generator=g, device="cuda").to(td),
+                         (torch.randn((R, W, cfg.Hkv, cfg.D), generator=g, device="cuda") * s).to(td),
+                         (torch.randn((R, W, cfg.Hkv, cfg.D), generator=g, device="cuda") * s).to(td))
+                        for _ in range(cfg.layers)]
+        return self.box
+
 
 def lm_head_bench(args):
     """The output head fused with the decoding step (bs_lm_head_decode) against
@@ -555,7 +567,8 @@ def serve_bench(args):
     policy = bs.SCHED_FIXED if args.policy == "fixed" else bs.SCHED_BUDGET
     rows = B if policy == bs.SCHED_FIXED else args.rows
     cfg = serve.ServeConfig(L=32, layers=args.layers, Hq=32, Hkv=32, D=128, V=126464, dtype="bf16", rows=rows,
-                            width=W, policy=policy, budget=budget, fixed_batch=B, tau=0.9, q_min=1, eos_id=-1)
+                            width=W, policy=policy, budget=budget, fixed_batch=B, tau=0.9, q_min=1, eos_id=-1,
+                            refresh=args.refresh, rope_base=synth.ROPE_BASE[2] if args.refresh else 0.0)
     print(f"[bench] serving {args.serve} x{len(stream)} ({args.policy}, B={B}, budget={budget}, rows={rows}, W={W})",
           file=sys.stderr, flush=True)
     prov = DeviceProvider(cfg)
@@ -574,11 +587,12 @@ def serve_bench(args):
         "n_gpus": 1, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"serve-{args.serve}-llada8b-layer", "requests": len(stream), "policy": args.policy,
                    "baseline_batch": B, "budget_tokens": budget, "rows": rows, "W": W, "layers": args.layers,
-                   "stream": "prompt/generated lengths shaped like the benchmark statistics table row"},
+                   "stream": "prompt/generated lengths shaped like the benchmark statistics table row",
+                   "dual_cache_refresh": bool(args.refresh)},
         "wall_s": round(wall, 3), "block_cycles": res.cycles, "denoising_steps": res.steps,
         "generated_tokens": gen, "steps_per_cycle": round(res.steps / res.cycles, 2),
         "mean_active": round(sum(res.active_counts) / res.cycles, 2), "R_eq2": round(R, 3),
-        "ms_per_step": round(wall * 1e3 / res.steps, 4)}), flush=True)
+        "ms_per_step": round(wall * 1e3 / res.steps, 4), "refresh_calls": res.refreshes}), flush=True)
 
 
 def main():
@@ -606,7 +620,8 @@ def main():
     ap.add_argument("--lm-head", action="store_true",
                     help="time the output head fused with the decoding step against the unfused GEMM + decode")
     ap.add_argument("--refresh", action="store_true",
-                    help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer")
+                    help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer; "
+                         "with --serve, rebuild the dual cache at every block start of the serving loop")
     ap.add_argument("--no-library", action="store_true", help="--refresh: skip the library attention comparison")
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
@@ -618,7 +633,7 @@ def main():
             sys.exit(2)
         lm_head_bench(args)
         return
-    if args.refresh and not args.traffic_summary:
+    if args.refresh and not args.traffic_summary and not args.serve:
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
                   file=sys.stderr, flush=True)

@@ -6,10 +6,14 @@ Each iteration is one block-cycle:
 2. admitted requests' prefilled KV rows are copied from a staging box into
    their rows of the dense KV box (K4, stable slots) and their token / mask
    rows are written;
-3. denoising steps run on the fused step entry point until every active
+3. with `refresh` on, the dual cache is rebuilt first: for every layer the
+   provider's projections of the whole box go through the refresh entry
+   point (rotary embedding at the rows' position ids, keys and values into
+   the cache, full-row attention), which also prefills the admitted rows;
+4. denoising steps run on the fused step entry point until every active
    request's block is fully unmasked (at most L steps, since every step
    unmasks at least one masked position of each block);
-4. the scheduler advances every request by one block and evicts those that
+5. the scheduler advances every request by one block and evicts those that
    reached K_i blocks or reported EOS during the cycle; their rows are read
    back as the requests' outputs.
 
@@ -23,6 +27,9 @@ prefilled KV and prompt tokens at admission) comes from a provider object:
     provider.step(ids, descs, cycle, step) -> (layers, logits)
         layers: per layer (q, k_new, v_new) device tensors [n][L][H][D];
         logits: [n][L][V] device tensor (row stride a multiple of 16 bytes).
+    provider.refresh(ids, descs, cycle) -> layers       (with `refresh` on)
+        per layer (q, k, v) device tensors [R][W][H][D]: the projections of
+        the whole box at the block start (bf16, D = 128).
 
 PyTorch only supplies device memory and the stream; every step runs in the
 library's kernels, and every scheduling decision in its native scheduler.
@@ -34,8 +41,8 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-from . import (SCHED_BUDGET, Context, Scheduler, bs_decode_workspace_bytes, bs_kv_scatter_compact,
-               bs_mixed_state_step)
+from . import (SCHED_BUDGET, Context, Scheduler, bs_decode_workspace_bytes, bs_dual_cache_refresh,
+               bs_kv_scatter_compact, bs_mixed_state_step)
 from .step import dt_code, torch_dtype
 
 
@@ -58,6 +65,8 @@ class ServeConfig:
     q_min: int = 1
     eos_id: int = -1
     mask_id: int = 0
+    refresh: bool = False    # rebuild the dual cache at every block start (bf16, D = 128)
+    rope_base: float = 0.0   # rotary base of the refresh (<= 0: no rotation)
 
 
 @dataclass
@@ -66,6 +75,7 @@ class ServeResult:
     blocks: dict = field(default_factory=dict)      # id -> block-cycles spent active
     cycles: int = 0
     steps: int = 0
+    refreshes: int = 0                              # refresh calls (one per layer and cycle)
     active_counts: list = field(default_factory=list)
     admitted: list = field(default_factory=list)    # per cycle
     evicted: list = field(default_factory=list)     # per cycle
@@ -89,6 +99,10 @@ class Server:
         self.ws = torch.empty(max(bs_decode_workspace_bytes(R, cfg.L, cfg.V, dt_code(cfg.dtype)), 16),
                               dtype=torch.uint8, device=device)
         self.info = {}      # id -> (p, g)
+        if cfg.refresh:
+            if cfg.dtype != "bf16" or cfg.D != 128:
+                raise ValueError("the dual-cache refresh runs in bf16 with D = 128")
+            self.ref_out = torch.empty((R, W, cfg.Hq, cfg.D), dtype=td, device=device)
 
     def _admit(self, plan):
         ids = plan["admitted"]
@@ -135,6 +149,11 @@ class Server:
             if n == 0:
                 break
             self._admit(plan)
+            if cfg.refresh:
+                for l, (q, k, v) in enumerate(self.provider.refresh(ids, descs, res.cycles)):
+                    bs_dual_cache_refresh(self.ctx, descs, cfg.L, cfg.Hq, cfg.Hkv, cfg.D, dt, 0.0, cfg.rope_base,
+                                          q, k, v, cfg.rows, cfg.width, self.k_box[l], self.v_box[l], self.ref_out)
+                    res.refreshes += 1
             res.admitted.append(plan["admitted"].tolist())
             res.active_counts.append(n)
             eos_any = np.zeros(n, np.uint8)

@@ -16,7 +16,10 @@ event with it (the step's own dirty lines are written back inside the
 region). A second region of K steps arms the library's
 event ring, which records the phase times (attention over all layers, decode
 row reductions, selection) on the same stream; the roofline's launch duration
-comes from it. The ring's events cost a few microseconds each, so they are
+comes from it. A third region repeats the steps without the sweep (the warm
+number, reported alongside), and a plain device copy of the step's byte count
+is timed the same way as a reference. `--config 5` times the 32-layer churn
+step (compaction, then the fused step) with device-drawn inputs. The ring's events cost a few microseconds each, so they are
 kept out of the headline region. Prints ONE JSON line: positions/s, ms per step, phase times,
 algorithmic HBM traffic, the roofline of the dominant kernel and the CPU oracle
 timed on a bounded sample of the same workload.
@@ -550,6 +553,154 @@ def refresh_bench(args):
     print(json.dumps(res), flush=True)
 
 
+def churn_bench(args):
+    """Workload 5, the LLaDA-8B-shaped 32-layer batch at a block boundary: one
+    step is K4 (the admitted requests' staged KV copied into the freed rows of
+    every layer, stable slots) followed by the fused step (attention in all 32
+    layers, then the decode) on the post-churn descriptors. The churn plan,
+    token and mask state come from the seeded generators; the 52 GB of KV,
+    the per-layer queries and fresh KV and the logits are drawn on the device
+    from a seeded torch generator with the same distributions (host
+    generation at this size would take longer than the run). Repeating the
+    step is idempotent for the KV (the same rows are copied and written
+    through again); the token/mask state is restored between steps. Prints
+    one JSON line."""
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+    from paper_2607_08930_amd import step as bstep
+
+    torch.cuda.set_device(0)
+    w = synth.workload(5)
+    tok, msk, _ = synth.gen_state(w)
+    plan = synth.churn_plan(w, w.reqs, tok, msk, step=1)          # rewrites tok/msk rows in place
+    w.reqs = plan.reqs
+    n, R, W, NL, L = w.n, w.R, w.W, w.layers, w.L
+    print(f"[bench] {w.name}: {n} requests, {NL} layers, {len(plan.segs)} copy segments; drawing inputs",
+          file=sys.stderr, flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(260708930)
+    td, s = torch.bfloat16, 1.0 / np.sqrt(w.D)
+
+    def normal(shape, sigma):
+        return (torch.randn(shape, generator=g, device="cuda") * sigma).to(td)
+
+    kbox = torch.empty((NL, R, w.Hkv, W, w.D), dtype=td, device="cuda")
+    vbox = torch.empty_like(kbox)
+    for l in range(NL):
+        kbox[l] = normal((R, w.Hkv, W, w.D), s)
+        vbox[l] = normal((R, w.Hkv, W, w.D), s)
+    n_adm = len(plan.stage_reqs)
+    wst = int((plan.stage_reqs["p"] + plan.stage_reqs["g"]).max()) if n_adm else 1
+    stg_k = normal((NL, max(n_adm, 1), w.Hkv, wst, w.D), s)
+    stg_v = normal((NL, max(n_adm, 1), w.Hkv, wst, w.D), s)
+    layers = [bstep.Layer(normal((n, L, w.Hq, w.D), 1.0), normal((n, L, w.Hkv, w.D), s),
+                          normal((n, L, w.Hkv, w.D), s), kbox[l], vbox[l],
+                          torch.empty((n, L, w.Hq, w.D), dtype=td, device="cuda")) for l in range(NL)]
+    x = torch.randn((n * L, w.V), generator=g, device="cuda")     # spiked logits (max probability around tau)
+    sid = torch.randint(1, w.V, (n * L,), generator=g, device="cuda")
+    m = torch.rand((n * L,), generator=g, device="cuda") * 8.0
+    x.scatter_(1, sid[:, None], (torch.logsumexp(x, dim=1) + m)[:, None])
+    logits = x.view(n, L, w.V).to(td)
+    del x
+    st = bstep.StepState(L, w.Hq, w.Hkv, w.D, w.V, w.dtype, R, W, bstep.to_device(tok), bstep.to_device(msk),
+                         layers, logits, n, tau=w.tau, q_min=w.q_min, eos_id=w.eos_id).alloc()
+    tok0, msk0 = st.tokens.clone(), st.mask.clone()
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    ctx = bs.Context(0)
+
+    def one_step():
+        bstep.compact(ctx, plan.segs, NL, w.Hkv, w.D, w.dtype, kbox, vbox, stg_k, stg_v, kbox, vbox, stream=stream)
+        bstep.run_step(ctx, st, w.reqs, stream=stream)
+
+    def reset():
+        st.tokens.copy_(tok0)
+        st.mask.copy_(msk0)
+        flush.sum()
+
+    for _ in range(args.warmup):
+        reset()
+        one_step()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(args.steps):
+        reset()
+        e0, e1 = region_events()
+        e0.record(stream)
+        one_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ctx.close()
+    ms = float(np.median(times))
+    ab = algorithmic_bytes(w)
+    nmask = 0
+    for r, (s0, B, _) in zip(w.reqs, w.spans()):
+        nmask += int(np.count_nonzero(msk[int(r["row"]), int(r["off"]) + s0:int(r["off"]) + s0 + B]))
+    copied = int(plan.segs["len"].sum()) if len(plan.segs) else 0
+    copy_bytes = 2 * copied * w.Hkv * w.D * 2 * w.elem * NL
+    small = ab["positions"] * (4 + 4 + 1 + 1 + 4)
+    step_bytes = ab["attn"] + nmask * w.V * w.elem + copy_bytes + small
+    gbs = step_bytes / (ms / 1e3) / 1e9
+    res = {
+        "metric": "denoised block positions/s per mixed-state step", "value": round(ab["positions"] / (ms / 1e3), 1),
+        "unit": "positions/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (KV, queries and logits drawn on the device)",
+        "config": {"workload": w.name, "n_requests": n, "layers": NL, "positions_per_step": ab["positions"],
+                   "masked_rows": nmask, "copied_tokens": copied, "admitted": n_adm, "finished": plan.n_finish,
+                   "cache": "cold (52 GB of KV; 512 MiB read sweep between steps)"},
+        "hbm": {"algorithmic_bytes_per_step": step_bytes, "achieved_GBps": round(gbs, 1),
+                "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+                "parts": {"attention_all_layers": ab["attn"], "logits": nmask * w.V * w.elem,
+                          "compaction": copy_bytes, "token_mask_pos": small}},
+        "step_ms_p10_p90": [round(float(np.percentile(times, 10)), 5), round(float(np.percentile(times, 90)), 5)],
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        print("[bench] timing the CPU oracle on a sample of the same workload", file=sys.stderr, flush=True)
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = 1
+        sample = list(range(8))
+        q = synth.gen_q(w, 0)
+        kn, vn = synth.gen_kv_new(w, 0)
+        kc = np.zeros((R, w.Hkv, W, w.D), np.uint16)
+        vc = np.zeros_like(kc)
+        for i in sample:
+            kc[int(w.reqs[i]["row"])], vc[int(w.reqs[i]["row"])] = synth.gen_cache_row(w, 0, int(w.reqs[i]["row"]))
+        blk = np.zeros((n, L), bool)
+        tok_c = np.zeros((n, L), np.int32)
+        msk_c = np.zeros((n, L), np.uint8)
+        lg = np.zeros((n, L, w.V), np.uint16)
+        for i in sample:
+            r = w.reqs[i]
+            s0, B, _ = w.spans()[i]
+            c0 = int(r["off"]) + s0
+            msk_c[i, :B] = msk[int(r["row"]), c0:c0 + B]
+            tok_c[i, :B] = tok[int(r["row"]), c0:c0 + B]
+            for j in range(B):
+                if msk_c[i, j]:
+                    lg[i, j] = synth.gen_logits_row(w, i, j)
+        t0 = time.perf_counter()
+        oracle.dual_cache_block_attention(w.reqs, L, q, kn, vn, kc, vc, dtype="bf16", only=sample)
+        t_att = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.parallel_decode(w.reqs, L, lg, tok_c, msk_c, tau=w.tau, q_min=w.q_min, eos_id=w.eos_id,
+                               dtype="bf16", only=sample)
+        t_dec = time.perf_counter() - t0
+        pos = sum(w.spans()[i][1] for i in sample)
+        t_step = t_att * NL + t_dec
+        res["cpu_baseline"] = {"value": round(pos / t_step, 1), "unit": "positions/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"{len(sample)} requests: one layer's attention ({t_att:.2f} s) scaled to "
+                                         f"{NL} layers, plus their decode ({t_dec:.2f} s); compaction not counted"}
+    print(json.dumps(res), flush=True)
+
+
 def serve_bench(args):
     """Closed-loop serving of a stream shaped like one row of the benchmark
     statistics table; prints one JSON line."""
@@ -598,9 +749,10 @@ def serve_bench(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload 1-4 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped)")
+    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped, 4 = skewed Dream batch, "
+                         "5 = 32-layer LLaDA churn step with compaction)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
     ap.add_argument("--pmc-calibration", action="store_true",
@@ -632,6 +784,13 @@ def main():
                   file=sys.stderr, flush=True)
             sys.exit(2)
         lm_head_bench(args)
+        return
+    if args.config == 5 and not args.traffic_summary and not args.serve:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        churn_bench(args)
         return
     if args.refresh and not args.traffic_summary and not args.serve:
         if args.gpus != 1:
@@ -693,10 +852,12 @@ def main():
     def one_step():
         bstep.run_step(ctx, st, w.reqs, stream=stream)
 
+    sweep = [not args.warm]
+
     def reset():
         st.tokens.copy_(tok0)
         st.mask.copy_(msk0)
-        if not args.warm:
+        if sweep[0]:
             flush.sum()
 
     for _ in range(args.warmup):
@@ -727,6 +888,10 @@ def main():
     step_ms, wall, _ = timed(False)
     # phase durations, live, over a second timed region of the same steps
     ring_ms, _, phases = timed(True)                  # [steps][attention, decode_rows, decode_select]
+    # the warm number alongside: the same steps without the cache sweep
+    sweep[0] = False
+    warm_ms, _, _ = timed(False)
+    sweep[0] = not args.warm
     ms = float(np.median(step_ms))
     attn_ms = float(np.median(phases[:, 0])) / w.layers       # one attention launch
     rows_ms = float(np.median(phases[:, 1]))
@@ -773,10 +938,13 @@ def main():
                    "layers": w.layers, "sum_len": int((w.reqs["p"] + w.reqs["g"]).sum()),
                    "cache": "warm" if args.warm else "cold (512 MiB read sweep between steps)"},
         "hbm": {"algorithmic_bytes_per_step": step_bytes, "achieved_GBps": round(step_bytes / (ms / 1e3) / 1e9, 1),
-                "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
+                "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                "frac_of_copy_reference": round(copy_ms / ms, 4)},
+        "ms_per_step_warm": round(float(np.median(warm_ms)), 5),
         "phases_ms": {n_: round(float(np.median(phases[:, i])), 5) for i, n_ in enumerate(bs.PROFILE_PHASES)},
         "kernel_GBps": {"attention": round(attn_gbs, 1), "decode_rows": round(dec_gbs, 1)},
         "attention_tflops": round(ab["attn_flops"] / w.layers / (attn_ms / 1e3) / 1e12, 2),
+        "attention_mfma_frac": round(ab["attn_flops"] / w.layers / (attn_ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
         "wall_ms_per_step_incl_restore": round(wall, 5),
         "step_ms_p10_p90": [round(float(np.percentile(step_ms, 10)), 5), round(float(np.percentile(step_ms, 90)), 5)],
         "ms_per_step_with_phase_events": round(float(np.median(ring_ms)), 5),

@@ -170,6 +170,15 @@ def test_decode_tiny_vocab_tail(ctx):
     _decode_case(ctx, w, "V=70000 bf16 (3 chunks, ragged)")
 
 
+def test_decode_largest_block_and_vocabulary(ctx):
+    # L = 64 (the largest block the selection handles: one lane per position)
+    # with a 262 144-entry bf16 vocabulary (8 parts of 64 KiB per row) and a
+    # ragged 262 147-entry one
+    for V in (262144, 262147):
+        w = synth.custom(64, 2, 2, 16, V, "bf16", [5, 40, 0], [128, 64, 70], [1, 0, 1])
+        _decode_case(ctx, w, f"L=64 V={V}")
+
+
 def test_decode_workspace_contents_ignored(ctx):
     # the workspace carries part results between the call's two launches only:
     # garbage on entry (NaN bit patterns, stale results of another step) must
@@ -259,6 +268,19 @@ def test_attention_edge_geometries(ctx):
                                             rows=[2, 0, 1], kv_sigma=0.1, q_sigma=3.0)),
         ("bf16 G8 L64 split", synth.custom(64, 16, 2, 64, 10, "bf16", [77, 5], [200, 64], [3, 0],
                                             kv_sigma=0.1)),
+    ]
+    for label, w in cases:
+        _att(ctx, w, label)
+
+
+def test_attention_long_rows(ctx):
+    # rows far longer than the workloads': 16 384 keys for MHA (512 tiles of a
+    # single wave's stream) and 12 000 for a 7-head group, next to short rows
+    cases = [
+        ("bf16 MHA 16384", synth.custom(32, 4, 4, 128, 10, "bf16", [16000, 7], [384, 40], [5, 1],
+                                         kv_sigma=0.1, q_sigma=2.0)),
+        ("bf16 G7 12000", synth.custom(32, 14, 2, 128, 10, "bf16", [11488, 90], [512, 64], [15, 1],
+                                        kv_sigma=0.1, q_sigma=2.0)),
     ]
     for label, w in cases:
         _att(ctx, w, label)

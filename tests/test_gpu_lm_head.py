@@ -115,6 +115,17 @@ def test_lm_head_row_tile_orders(ctx, n):
     assert nex <= n // 8
 
 
+def test_lm_head_largest_row_count(ctx):
+    # n * L = 65536, the most the call accepts: 1024 requests with 64-position
+    # blocks (about 32k masked rows, 128 row tiles); a seeded sample of 64
+    # requests is checked against the oracle
+    n = 1024
+    w = synth.custom(64, 2, 2, 16, 300, "bf16", [3 + i % 17 for i in range(n)], [64] * n, [0] * n)
+    sample = sorted(np.random.default_rng(9).choice(n, size=64, replace=False).tolist())
+    _, _, nex, _ = lm_case(ctx, w, 32, "n*L=65536", sample=sample)
+    assert nex <= len(sample) // 8
+
+
 @pytest.mark.parametrize("cfg", [2, 3])
 def test_lm_head_full_size_sampled(ctx, cfg):
     w = synth.workload(cfg)

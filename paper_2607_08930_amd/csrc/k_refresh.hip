@@ -253,28 +253,33 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
     wait_vm_c<0>();
   __syncthreads();
 
-  f32x16_t sc[QW], sn[QW];
-  bf16x8_t pprev[QW][2], pcur[QW][2];
+  // two sets of score and probability registers, used in turn by the two
+  // halves of each loop trip (no register copies between sub-tiles)
+  f32x16_t sA[QW], sB[QW];
+  bf16x8_t pA[QW][2], pB[QW][2];
 #pragma unroll
   for (int b = 0; b < QW; ++b)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pprev[b][ks][e] = (__bf16)0.0f;
+      for (int e = 0; e < 8; ++e) pA[b][ks][e] = (__bf16)0.0f;
   if (active) {
 #pragma unroll
     for (int b = 0; b < QW; ++b)
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) sc[b][rr] = 0.0f;
+      for (int rr = 0; rr < 16; ++rr) sA[b][rr] = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(ring + koff[kk]);
 #pragma unroll
-      for (int b = 0; b < QW; ++b) sc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qb[b][kk], sc[b], 0, 0, 0);
+      for (int b = 0; b < QW; ++b) sA[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qb[b][kk], sA[b], 0, 0, 0);
     }
   }
 
-  for (int u = 0; u < nsub; ++u) {
+  // one sub-tile u: sc holds its scores, pprev the probabilities of u - 1;
+  // writes the scores of u + 1 to sn and the probabilities of u to pcur
+  auto sub_tile = [&](int u, f32x16_t (&sc)[QW], f32x16_t (&sn)[QW], const bf16x8_t (&pprev)[QW][2],
+                      bf16x8_t (&pcur)[QW][2]) {
     const int un = u + 1;
     if (un < nsub && (un & 1) == 0) {
       // sub-tile un opens tile T: it has landed once only tile T + 1 (if
@@ -287,19 +292,19 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
       __syncthreads();
       if (T + 2 < ntiles) issue(T + 2);
     }
-    if (!active) continue;
-    // a reference max raised in the previous iteration rescales the
+    if (!active) return;
+    // a reference max raised in the previous sub-tile rescales the
     // accumulators now, after P V of its predecessor and before its own (at
-    // the top of the body, so the loop's tail stays one basic block in which
-    // the exponentials and the MFMAs can interleave)
+    // the top, so the tail stays one basic block in which the exponentials
+    // and the MFMAs can interleave)
     if (resc_pend) {
       rescale();
       resc_pend = false;
     }
-    // K fragments of sub-tile u + 1 (on the last iteration a resident one
+    // K fragments of sub-tile u + 1 (on the last sub-tile a resident one
     // again, its scores discarded), issued first so their latency hides under
-    // the softmax arithmetic; V of u - 1 (of sub-tile 0 on the first
-    // iteration, with zero weights)
+    // the softmax arithmetic; V of u - 1 (of sub-tile 0 at u = 0, with zero
+    // weights)
     const uint16_t* kt = ring + sub_k(un < nsub ? un : u);
     const uint16_t* vs = ring + sub_k(u > 0 ? u - 1 : 0) + TILE;
     bf16x8_t kf[NKK];
@@ -341,8 +346,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
       const float nm = -mrun[b];
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[b][rr], a.scale_log2e, nm));
-        pcur[b][rr >> 3][rr & 7] = (__bf16)p;
+        const float pr = __builtin_amdgcn_exp2f(fmaf(sc[b][rr], a.scale_log2e, nm));
+        pcur[b][rr >> 3][rr & 7] = (__bf16)pr;
       }
       lsum[b] = add_weights(add_weights(lsum[b], pcur[b][0]), pcur[b][1]);
     }
@@ -370,11 +375,19 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
     }
+  };
+
+  int u = 0;
+  for (; u + 1 < nsub; u += 2) {
+    sub_tile(u, sA, sB, pA, pB);
+    sub_tile(u + 1, sB, sA, pB, pA);
+  }
+  if (u < nsub) {                                   // odd count: the last sub-tile's probabilities end in pB
+    sub_tile(u, sA, sB, pA, pB);
 #pragma unroll
     for (int b = 0; b < QW; ++b) {
-      sc[b] = sn[b];
-      pprev[b][0] = pcur[b][0];
-      pprev[b][1] = pcur[b][1];
+      pA[b][0] = pB[b][0];
+      pA[b][1] = pB[b][1];
     }
   }
   if (!active) return;
@@ -388,7 +401,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
         const bf16x8_t va = vfrag(vs, dt, ks);
 #pragma unroll
         for (int b = 0; b < QW; ++b)
-          o[b][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pprev[b][ks], o[b][dt], 0, 0, 0);
+          o[b][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pA[b][ks], o[b][dt], 0, 0, 0);
       }
   }
 

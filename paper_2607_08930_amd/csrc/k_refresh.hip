@@ -111,7 +111,7 @@ __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
 // MFMAs but needs about 400 registers (one wave per SIMD, so nothing hides
 // the softmax arithmetic and the LDS latency: 20% slower on the Dream-7B
 // shape); QW = 1 reads twice the LDS bytes per MFMA and fits two waves per
-// SIMD (209 VGPRs), which is what the launch uses.
+// SIMD (222 VGPRs), which is what the launch uses.
 template <int D, int QW, int NW>
 __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
   static_assert(D == 128, "the refresh attention is laid out for D = 128");

@@ -200,6 +200,48 @@ def test_decode_workspace_contents_ignored(ctx):
         tok_c, msk_c = got["tokens"], got["masked"]
 
 
+def test_decode_same_requests_on_two_streams(ctx):
+    # calls with the same descriptors share the library's uploaded copy of
+    # them; enqueued on two streams with no host sync in between (each with its
+    # own workspace), each must still select exactly as the oracle does, also
+    # with a batch of another size between them
+    torch, bs, bstep = lazy()
+    w = synth.workload(2, V=70000)
+    tok, msk, blk = synth.gen_state(w)
+    tok_c, _ = oracle.gather_active_blocks(w.reqs, w.L, tok)
+    msk_c, _ = oracle.gather_active_blocks(w.reqs, w.L, msk)
+    logits = synth.gen_logits(w, blk)
+    ref = oracle.parallel_decode(w.reqs, w.L, logits, tok_c, msk_c, tau=w.tau, q_min=1, eos_id=-1, dtype=w.dtype)
+    sub = w.reqs[:5]
+    ref_sub = oracle.parallel_decode(sub, w.L, logits[:5], tok_c[:5], msk_c[:5], tau=w.tau, q_min=1, eos_id=-1,
+                                     dtype=w.dtype)
+    dl = bstep.to_device(logits, w.dtype)
+    dtc = bstep.dt_code(w.dtype)
+    wsb = bs.bs_decode_workspace_bytes(w.n, w.L, w.V, dtc)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    runs = []
+    for k, (st, reqs) in enumerate([(0, w.reqs), (1, w.reqs), (0, sub), (1, w.reqs), (0, w.reqs)]):
+        n = len(reqs)
+        say(f"[decode streams call {k}] stream={st} n={n}")
+        o = dict(tokens=bstep.to_device(tok_c[:n]), masked=bstep.to_device(msk_c[:n]),
+                 n_unmasked=torch.full((n,), -7, dtype=torch.int32, device="cuda"),
+                 done=torch.full((n,), 7, dtype=torch.uint8, device="cuda"),
+                 eos_seen=torch.full((n,), 7, dtype=torch.uint8, device="cuda"),
+                 conf=torch.full((n, w.L), float("nan"), dtype=torch.float32, device="cuda"),
+                 ws=torch.full((wsb,), 0xFF, dtype=torch.uint8, device="cuda"))
+        torch.cuda.synchronize()                   # inputs in place before the other streams read them
+        s = streams[st]
+        bs.bs_parallel_decode(ctx, reqs, w.L, w.V, dtc, dl, dl.stride(1), o["tokens"], o["masked"], w.tau, 1, -1,
+                              o["n_unmasked"], o["done"], o["eos_seen"], o["conf"], o["ws"], wsb,
+                              stream=s.cuda_stream)
+        runs.append((n, o))
+    torch.cuda.synchronize()
+    for k, (n, o) in enumerate(runs):
+        got = {key: v.cpu().numpy() for key, v in o.items() if key != "ws"}
+        check_decode(w, got, ref if n == w.n else ref_sub, reqs=w.reqs if n == w.n else sub,
+                     label=f"streams call {k}")
+
+
 def test_decode_rejects_unaligned_row_stride(ctx):
     torch, bs, bstep = lazy()
     w = synth.custom(8, 2, 2, 16, 300, "bf16", [3], [16], [1])

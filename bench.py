@@ -78,6 +78,29 @@ def build_state(w, dev_logits_fill=True):
     return st, dict(tokens=tok, mask=msk, blk=blk, layers=host, logits=logits)
 
 
+def deeper_state(w, st, layers):
+    """Adds layers 1 .. layers-1 to a one-layer step: each gets its own device
+    tensors of layer 0's shapes and value distributions (queries and fresh
+    block K/V ~ N(0, 1), cached K/V ~ N(0, 1/D)), drawn on the device. The
+    whole-depth step then runs attention once per layer, then one decode."""
+    import torch
+    from paper_2607_08930_amd import step as bstep
+    g = torch.Generator(device="cuda").manual_seed(1000 + w.cfg)
+    l0 = st.layers[0]
+
+    def draw(like, sigma):
+        x = torch.empty(like.shape, dtype=torch.float32, device="cuda").normal_(0.0, sigma, generator=g)
+        return x.to(like.dtype)
+
+    for _ in range(1, layers):
+        st.layers.append(bstep.Layer(draw(l0.q, 1.0), draw(l0.k_new, 1.0), draw(l0.v_new, 1.0),
+                                     draw(l0.k_cache, w.D ** -0.5), draw(l0.v_cache, w.D ** -0.5),
+                                     torch.empty_like(l0.out)))
+    torch.cuda.synchronize()
+    w.layers = layers
+    w.name += f"-depth{layers}"
+
+
 def masked_rows(blk):
     return int(blk.sum())
 
@@ -766,7 +789,9 @@ def main():
     ap.add_argument("--batch", type=int, default=16, help="fixed cap, and B of Eq. 2")
     ap.add_argument("--budget", type=int, default=0, help="Eq. 1 budget in tokens (default B * (avg prompt + limit))")
     ap.add_argument("--rows", type=int, default=128, help="rows of the dense box under the budget policy")
-    ap.add_argument("--layers", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=1,
+                    help="attention layers per step (step mode: layers past the first are drawn on the device; "
+                         "--serve: model depth)")
     ap.add_argument("--block-length", type=int, default=None,
                     help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
     ap.add_argument("--lm-head", action="store_true",
@@ -833,6 +858,8 @@ def main():
         w.name += "-prefix-only"
     print(f"[bench] building inputs for {w.name}", file=sys.stderr, flush=True)
     st, host = build_state(w)
+    if args.layers > 1:
+        deeper_state(w, st, args.layers)
     ab = algorithmic_bytes(w)
     nmask = masked_rows(host["blk"])
     logits_bytes = nmask * w.V * w.elem
@@ -953,7 +980,7 @@ def main():
                            "what": "device copy of the step's byte count (half read, half written), cold"},
         "roofline": roof,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.layers == 1:
         print("[bench] timing the CPU oracle on the same inputs", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, host)
     print(json.dumps(res), flush=True)

@@ -19,7 +19,9 @@ row reductions, selection) on the same stream; the roofline's launch duration
 comes from it. A third region repeats the steps without the sweep (the warm
 number, reported alongside), and a plain device copy of the step's byte count
 is timed the same way as a reference. `--config 5` times the 32-layer churn
-step (compaction, then the fused step) with device-drawn inputs. The ring's events cost a few microseconds each, so they are
+step (compaction, then the fused step) with device-drawn inputs; `--layers N`
+gives the one-layer workloads N attention layers (layers past the first
+drawn on the device) before their one decode. The ring's events cost a few microseconds each, so they are
 kept out of the headline region. Prints ONE JSON line: positions/s, ms per step, phase times,
 algorithmic HBM traffic, the roofline of the dominant kernel and the CPU oracle
 timed on a bounded sample of the same workload.

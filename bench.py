@@ -657,9 +657,19 @@ def churn_bench(args):
         e1.record(stream)
         torch.cuda.synchronize()
         times.append(e0.elapsed_time(e1))
+    # phase durations, live, over a second region of the same steps (the
+    # library's event ring brackets the 32 attention launches and the decode)
+    bs.bs_profile_begin(ctx, args.steps)
+    for _ in range(args.steps):
+        reset()
+        one_step()
+    torch.cuda.synchronize()
+    phases = bs.bs_profile_end(ctx, args.steps)
     ctx.close()
     ms = float(np.median(times))
     ab = algorithmic_bytes(w)
+    attn_ms = float(np.median(phases[:, 0])) / NL           # per launch, gaps between launches included
+    attn_gbs = ab["attn_per_layer"] / (attn_ms / 1e3) / 1e9
     nmask = 0
     for r, (s0, B, _) in zip(w.reqs, w.spans()):
         nmask += int(np.count_nonzero(msk[int(r["row"]), int(r["off"]) + s0:int(r["off"]) + s0 + B]))
@@ -681,6 +691,11 @@ def churn_bench(args):
                 "parts": {"attention_all_layers": ab["attn"], "logits": nmask * w.V * w.elem,
                           "compaction": copy_bytes, "token_mask_pos": small}},
         "step_ms_p10_p90": [round(float(np.percentile(times, 10)), 5), round(float(np.percentile(times, 90)), 5)],
+        "phases_ms": {n_: round(float(np.median(phases[:, i])), 5) for i, n_ in enumerate(bs.PROFILE_PHASES)},
+        "roofline": {"kernel": "k_attn_bf16_wave", "bound": "hbm", "achieved": round(attn_gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes_per_launch": ab["attn_per_layer"], "avg_launch_ms": round(attn_ms, 5),
+                     "traffic": read_traffic(w.name, "k_attn_bf16_wave")},
     }
     if not args.no_cpu_baseline:
         import oracle

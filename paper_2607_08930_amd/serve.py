@@ -94,8 +94,11 @@ class Server:
         self.v_box = torch.zeros_like(self.k_box)
         self.out = [torch.empty((R, cfg.L, cfg.Hq, cfg.D), dtype=td, device=device) for _ in range(cfg.layers)]
         self.n_unmasked = torch.empty(R, dtype=torch.int32, device=device)
-        self.done = torch.empty(R, dtype=torch.uint8, device=device)
-        self.eos_seen = torch.empty(R, dtype=torch.uint8, device=device)
+        # done and eos_seen side by side, so one small copy into pinned host
+        # memory brings both back after every step
+        self.flags = torch.zeros((2, R), dtype=torch.uint8, device=device)
+        self.flags_host = torch.zeros((2, R), dtype=torch.uint8, pin_memory=True)
+        self.done, self.eos_seen = self.flags[0], self.flags[1]
         self.ws = torch.empty(max(bs_decode_workspace_bytes(R, cfg.L, cfg.V, dt_code(cfg.dtype)), 16),
                               dtype=torch.uint8, device=device)
         self.info = {}      # id -> (p, g)
@@ -167,9 +170,11 @@ class Server:
                                     self.n_unmasked, self.done, self.eos_seen, None, None, self.ws,
                                     self.ws.numel())
                 res.steps += 1
-                flags = torch.stack((self.done[:n], self.eos_seen[:n])).cpu().numpy()
-                eos_any |= flags[1]
-                if flags[0].all():
+                self.flags_host.copy_(self.flags, non_blocking=True)
+                torch.cuda.current_stream().synchronize()
+                flags = self.flags_host.numpy()
+                eos_any |= flags[1, :n]
+                if flags[0, :n].all():
                     break
             evicted = self.sched.complete(eos_any)
             for rid in ids:

@@ -18,7 +18,10 @@ event ring, which records the phase times (attention over all layers, decode
 row reductions, selection) on the same stream; the roofline's launch duration
 comes from it. A third region repeats the steps without the sweep (the warm
 number, reported alongside), and a plain device copy of the step's byte count
-is timed the same way as a reference. `--config 5` times the 32-layer churn
+is timed the same way as a reference. A fourth region enqueues the K steps
+back to back between one pair of events (each step on its own token/mask copy,
+rotating over four copies of the layer inputs and logits so the data stays
+cold), with a back-to-back copy reference beside it. `--config 5` times the 32-layer churn
 step (compaction, then the fused step) with device-drawn inputs; `--layers N`
 gives the one-layer workloads N attention layers (layers past the first
 drawn on the device) before their one decode. The ring's events cost a few microseconds each, so they are
@@ -101,6 +104,73 @@ def deeper_state(w, st, layers):
     torch.cuda.synchronize()
     w.layers = layers
     w.name += f"-depth{layers}"
+
+
+B2B_SETS = 4      # input sets the back-to-back region rotates through
+
+
+def back_to_back(w, st, ctx, tok0, msk0, flush, stream, steps, reps=3):
+    """Median over `reps` regions of `steps` fused steps enqueued back to back
+    between one pair of HIP events (ms per step), and the host's enqueue time
+    per step. Returns (ms, host ms)."""
+    import dataclasses
+    import torch
+    from paper_2607_08930_amd import step as bstep
+    sets = [st]
+    for _ in range(B2B_SETS - 1):
+        lay = [bstep.Layer(x.q.clone(), x.k_new.clone(), x.v_new.clone(), x.k_cache.clone(), x.v_cache.clone(),
+                           torch.empty_like(x.out)) for x in st.layers]
+        sets.append(dataclasses.replace(st, layers=lay, logits=st.logits.clone()))
+    toks = [tok0.clone() for _ in range(steps)]
+    msks = [msk0.clone() for _ in range(steps)]
+    out, host = [], []
+    for rep in range(reps + 1):                       # the first region warms the enqueue path
+        for k in range(steps):
+            toks[k].copy_(tok0)
+            msks[k].copy_(msk0)
+        flush.sum()
+        torch.cuda.synchronize()
+        e0, e1 = region_events()
+        e0.record(stream)
+        t0 = time.perf_counter()
+        for k in range(steps):
+            s_ = sets[k % B2B_SETS]
+            s_.tokens, s_.mask = toks[k], msks[k]
+            bstep.run_step(ctx, s_, w.reqs, stream=stream)
+        t1 = time.perf_counter()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if rep:
+            out.append(e0.elapsed_time(e1) / steps)
+            host.append((t1 - t0) / steps * 1e3)
+    st.tokens, st.mask = sets[0].tokens, sets[0].mask
+    del sets, toks, msks
+    torch.cuda.synchronize()
+    return float(np.median(out)), float(np.median(host))
+
+
+def copy_back_to_back(nbytes, flush, stream, steps, reps=3):
+    """A plain device copy of nbytes (half read, half written) enqueued
+    `steps` times back to back over B2B_SETS buffer pairs: ms per copy."""
+    import torch
+    half = (nbytes // 2 + 255) // 256 * 256
+    pairs = [(torch.ones(half // 4, dtype=torch.float32, device="cuda"),
+              torch.empty(half // 4, dtype=torch.float32, device="cuda")) for _ in range(B2B_SETS)]
+    out = []
+    for rep in range(reps + 1):
+        flush.sum()
+        torch.cuda.synchronize()
+        e0, e1 = region_events()
+        e0.record(stream)
+        for k in range(steps):
+            src, dst = pairs[k % B2B_SETS]
+            dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if rep:
+            out.append(e0.elapsed_time(e1) / steps)
+    del pairs
+    return float(np.median(out))
 
 
 def masked_rows(blk):
@@ -936,6 +1006,12 @@ def main():
     sweep[0] = False
     warm_ms, _, _ = timed(False)
     sweep[0] = not args.warm
+    # back to back: K steps between one pair of events, as a serving loop
+    # runs them. Step k reads input set k % NB (copies of the layer inputs
+    # and logits at other addresses, so a set was last read NB - 1 steps and
+    # more than 1 GB of traffic before, cold in the Infinity Cache) and its
+    # own copy of the token/mask state, so every step does the same work.
+    b2b_ms, b2b_host_ms = back_to_back(w, st, ctx, tok0, msk0, flush, stream, args.steps)
     ms = float(np.median(step_ms))
     attn_ms = float(np.median(phases[:, 0])) / w.layers       # one attention launch
     rows_ms = float(np.median(phases[:, 1]))
@@ -972,6 +1048,7 @@ def main():
         copy_ms.append(e0.elapsed_time(e1))
     copy_ms = float(np.median(copy_ms))
     del csrc, cdst
+    copy_b2b_ms = copy_back_to_back(step_bytes, flush, stream, args.steps)
     res = {
         "metric": "denoised block positions/s per mixed-state step",
         "value": round(value, 1), "unit": "positions/s", "n_gpus": 1, "steps": args.steps,
@@ -985,6 +1062,12 @@ def main():
                 "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                 "frac_of_copy_reference": round(copy_ms / ms, 4)},
         "ms_per_step_warm": round(float(np.median(warm_ms)), 5),
+        "back_to_back": {"ms_per_step": round(b2b_ms, 5), "positions_per_s": round(ab["positions"] / (b2b_ms / 1e3), 1),
+                         "achieved_GBps": round(step_bytes / (b2b_ms / 1e3) / 1e9, 1),
+                         "frac_of_peak": round(step_bytes / (b2b_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                         "host_enqueue_ms_per_step": round(b2b_host_ms, 5),
+                         "copy_reference_ms": round(copy_b2b_ms, 5),
+                         "frac_of_copy_reference": round(copy_b2b_ms / b2b_ms, 4)},
         "phases_ms": {n_: round(float(np.median(phases[:, i])), 5) for i, n_ in enumerate(bs.PROFILE_PHASES)},
         "kernel_GBps": {"attention": round(attn_gbs, 1), "decode_rows": round(dec_gbs, 1)},
         "attention_tflops": round(ab["attn_flops"] / w.layers / (attn_ms / 1e3) / 1e12, 2),

@@ -602,7 +602,7 @@ def refresh_bench(args):
             prep_library()
             timed(library, max(1, args.warmup))
             lib_ms = timed(library, args.steps)
-        except RuntimeError as e:                 # no flash kernel for this shape on this build
+        except RuntimeError as e:                 # no flash kernel for this shape in this PyTorch
             print(f"[bench] library flash attention unavailable: {e}", file=sys.stderr, flush=True)
     ctx.close()
     tflops = flops / (att_ms / 1e3) / 1e12

@@ -73,7 +73,7 @@ typedef enum bs_dtype { BS_F32 = 0, BS_BF16 = 1 } bs_dtype;
 typedef enum bs_status {
   BS_OK = 0,
   BS_ERR_INVALID_ARG = 1,  /* null pointer, bad enum, negative size, bad stride */
-  BS_ERR_UNSUPPORTED = 2,  /* shape/dtype combination this build does not serve */
+  BS_ERR_UNSUPPORTED = 2,  /* shape/dtype combination the library does not serve */
   BS_ERR_DESCRIPTOR = 3,   /* descriptor array invalid (see conventions above) */
   BS_ERR_OVERLAP = 4,      /* copy destinations intersect, or a source aliases a destination */
   BS_ERR_WORKSPACE = 5,    /* workspace missing or smaller than the size query returns */

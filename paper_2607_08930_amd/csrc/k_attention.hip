@@ -149,13 +149,18 @@ __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
   for (int k = 0; k < 4; ++k) lsum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{p[2 * k], p[2 * k + 1]}, one, lsum, false);
   return lsum;
 }
-// XOR swizzle of a row's 16-byte slots. Rows r0..r0+3 (r0 % 4 == 0) differ in
-// bits 1..2, so the transpose reads of 4 consecutive keys x 2 chunks hit 8
-// distinct slots; any 16 consecutive rows get distinct slots for one chunk.
+// XOR swizzle of a row's 16-byte slots. D = 128 (16 slots), for an LDS that
+// serves 256 bytes (64 banks of 4 bytes) per cycle: the 32 lanes of one
+// transposed V read cover rows r0 .. r0 + 3 (r0 % 4 == 0) at chunks
+// 4 t .. 4 t + 3, and row bits 0..1 moved to slot bits 2..3 put them in 16
+// distinct slots; row bits 2..3 moved to slot bits 0..1 keep any 16
+// consecutive rows on distinct slots for one chunk (the K reads). D = 64
+// (8 slots): rows r0..r0+3 differ in bits 1..2 and any 8 consecutive rows get
+// distinct slots for one chunk.
 template <int NCH>
 __device__ inline int swz(int row) {
-  const int base = ((row & 3) << 1) | ((row >> 2) & 1);
-  return NCH == 16 ? (base | (row & 8)) : base;
+  if constexpr (NCH == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
+  return ((row & 3) << 1) | ((row >> 2) & 1);
 }
 
 // One (request, KV head) item processed by GW waves that share its K/V tiles:

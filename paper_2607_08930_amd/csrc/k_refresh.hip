@@ -90,11 +90,13 @@ __global__ __launch_bounds__(256) void k_refresh_kv(RefKvArgs a) {
 }
 
 // ------------------------------------------------------------------ attention
-// XOR swizzle of a cache row's 16-byte slots in LDS (D = 128: 16 slots): rows
-// r0 .. r0 + 3 differ in bits 1..2, so the transposed V reads of 4 consecutive
-// keys x 2 chunks hit 8 distinct slots, and any 16 consecutive rows get
-// distinct slots for one chunk (the K fragment reads).
-__device__ inline int swz16(int row) { return (((row & 3) << 1) | ((row >> 2) & 1)) | (row & 8); }
+// XOR swizzle of a cache row's 16-byte slots in LDS (D = 128: 16 slots) for
+// an LDS that serves 256 bytes (64 banks of 4 bytes) per cycle. The 32 lanes
+// of one transposed V read cover rows r0 .. r0 + 3 (r0 % 4 == 0) at chunks
+// 4 t .. 4 t + 3: row bits 0..1 move to slot bits 2..3, so those reads land
+// in 16 distinct slots; row bits 2..3 move to slot bits 0..1, so any 16
+// consecutive rows still get distinct slots for one chunk (the K reads).
+__device__ inline int swz16(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
 
 __device__ inline float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
 

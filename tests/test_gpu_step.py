@@ -97,6 +97,36 @@ def test_fused_step_matches_oracle(ctx, cfg):
     say(f"  exempt requests: {nex}")
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_fused_step_random_geometries(ctx, seed):
+    # seeded random batches: block length, head grouping, head dimension,
+    # vocabulary, prompt and generation lengths, block indices (partial last
+    # blocks, empty suffixes), row order with unused rows and padding slack
+    torch, bs, bstep = lazy()
+    g_ = np.random.default_rng(9000 + seed)
+    L = int(g_.choice([8, 16, 32, 64]))
+    Hq, Hkv = [(4, 4), (8, 2), (14, 2), (8, 1)][seed % 4]
+    D = 64 if seed % 3 == 0 else 128
+    V = 8 * int(g_.integers(40, 700))                 # rows stay a multiple of 16 bytes
+    n = int(g_.integers(1, 13))
+    p = g_.integers(0, 200, n)
+    gen = g_.integers(1, 200, n)
+    k = np.array([int(g_.integers(0, -(-int(x) // L))) for x in gen])
+    rows = g_.permutation(n + int(g_.integers(0, 4)))[:n]
+    W = int((p + gen).max()) + int(g_.integers(0, 24))
+    w = synth.custom(L, Hq, Hkv, D, V, "bf16", list(p), list(gen), list(k), W=W, rows=list(rows), variant=seed,
+                     kv_sigma=1 / D ** 0.5)
+    say(f"[fused step random {seed}] n={n} L={L} Hq={Hq} Hkv={Hkv} D={D} V={V} W={W} R={w.R}")
+    st, host = make_state(w)
+    bstep.run_step(ctx, st, w.reqs, want_conf=True)
+    torch.cuda.synchronize()
+    got = snapshot(st)
+    ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
+                                  tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+    nex = check_step(w, got, ref, host, f"random {seed}")
+    say(f"  exempt requests: {nex} of {n}")
+
+
 @pytest.mark.parametrize("cfg,L", [(2, 16), (2, 64), (3, 16), (3, 64)])
 def test_fused_step_block_length_sweep(ctx, cfg, L):
     """The block-length ablation at kernel level: the same LLaDA- and

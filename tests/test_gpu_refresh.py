@@ -117,6 +117,41 @@ def test_small_ragged_rows_in_full(ctx, Hq, Hkv, base):
     say(f"  max abs error {worst:.2e}")
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_random_geometries(ctx, seed):
+    # seeded random batches: head grouping, lengths 1..700 (ragged 64-key
+    # tiles and 256-query chunks), row order with unused rows, padding slack,
+    # rotary base; every request against the oracle, nothing else written
+    torch, bs, bstep = lazy()
+    g_ = np.random.default_rng(7000 + seed)
+    Hq, Hkv = [(4, 4), (8, 2), (14, 2), (8, 1), (6, 3), (7, 7)][seed]
+    base = [1e4, 5e5, 1e6, 0.0, 1e4, 5e5][seed]
+    n = int(g_.integers(1, 9))
+    p = g_.integers(0, 400, n)
+    gen = g_.integers(1, 300, n)
+    if seed % 2 == 0:                                  # a row shorter than one key tile
+        p[0], gen[0] = 0, int(g_.integers(1, 40))
+    rows = g_.permutation(n + int(g_.integers(0, 3)))[:n]
+    W = int((p + gen).max()) + int(g_.integers(0, 40))
+    w = synth.custom(32, Hq, Hkv, 128, 10, "bf16", list(p), list(gen), [0] * n, W=W, rows=list(rows),
+                     variant=seed, kv_sigma=1 / np.sqrt(128))
+    say(f"[refresh random {seed}] n={n} Hq={Hq} Hkv={Hkv} base={base} W={W} R={w.R} "
+        f"lens={[int(r['p'] + r['g']) for r in w.reqs]}")
+    q, k, v = synth.gen_refresh(w)
+    kc, vc = synth.poison_cache(w, *synth.gen_cache(w))
+    out, dkc, dvc = run_refresh(ctx, w, q, k, v, kc, vc, base)
+    out_h, kc_h, vc_h = bstep.to_host(out), bstep.to_host(dkc), bstep.to_host(dvc)
+    for i, r in enumerate(w.reqs):
+        row, off, ln = int(r["row"]), int(r["off"]), int(r["p"] + r["g"])
+        check_request(w, i, out_h[row, off:off + ln], kc_h[row, :, off:off + ln], vc_h[row, :, off:off + ln],
+                      q, k, v, base, label=f"random {seed}")
+    used = used_cells(w)
+    assert (out_h[~used] == synth.BF16_NAN).all()
+    for c in range(w.Hkv):
+        np.testing.assert_array_equal(kc_h[:, c][~used], kc[:, c][~used])
+        np.testing.assert_array_equal(vc_h[:, c][~used], vc[:, c][~used])
+
+
 def test_rotation_disabled_copies_keys(ctx):
     torch, bs, bstep = lazy()
     w = small_workload(4, 2, variant=1)

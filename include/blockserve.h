@@ -30,16 +30,20 @@
  * 16-bit words.
  *
  * Streams: `stream` is a hipStream_t (NULL = the legacy default stream). Every
- * call only enqueues work on it and never waits for the device; results are
- * valid after the stream (or an event recorded on it) has completed. Device
- * pointers must stay valid until then.
+ * call only enqueues work on it; results are valid after the stream (or an
+ * event recorded on it) has completed, and device pointers must stay valid
+ * until then. A call does not wait for the device, with one bounded
+ * exception: a context keeps the device copies of its descriptor sets in
+ * upload slots and adds a slot rather than overwrite one that queued work
+ * still reads; only when 256 distinct descriptor sets of one context are in
+ * flight at once does a call wait for the oldest of them to be read.
  *
  * Errors: every int-returning call returns a bs_status. Arguments are checked
  * on the host BEFORE anything is enqueued, so a failing call launches nothing
  * and leaves every tensor untouched; bs_last_error() gives the detail.
  *
- * Threads: a bs_ctx holds a ring of descriptor upload slots; use one context
- * per host thread. Calls on one context may target different streams.
+ * Threads: a bs_ctx holds the descriptor upload slots; use one context per
+ * host thread. Calls on one context may target different streams.
  */
 #ifndef BLOCKSERVE_H
 #define BLOCKSERVE_H
@@ -84,7 +88,8 @@ typedef struct bs_ctx bs_ctx;
 
 /* Create a context bound to HIP device `device` (it becomes current while the
  * library works). The context owns only pinned host staging memory and device
- * upload slots for descriptors and work lists. *out is NULL on failure. */
+ * upload slots for descriptors and work lists (allocated as calls need them).
+ * *out is NULL on failure. */
 int bs_create(bs_ctx** out, int device);
 
 /* Wait for every upload slot to drain, then free the context (NULL is OK). */
@@ -100,6 +105,16 @@ const char* bs_last_error(const bs_ctx* ctx);
 /* Host-only check of a descriptor array against block length L and an
  * R x W box (the rules under "Conventions"). Touches no device. */
 int bs_validate_requests(const bs_req_desc* reqs, int n, int L, int R, int W);
+
+/* Host-only check of a K4 segment array (the rules of bs_kv_scatter_compact
+ * below): every segment inside its boxes (source: R_src x W_src for src_kind
+ * 0, R_stg x W_stg for src_kind 1; destination R_dst x W_dst), destination
+ * ranges pairwise disjoint, and, when src_is_dst (stg_is_dst) is nonzero, no
+ * source range of that kind meeting any destination range. Segments of length
+ * 0 copy nothing and never overlap. Returns BS_OK, BS_ERR_INVALID_ARG or
+ * BS_ERR_OVERLAP (detail in bs_last_error(NULL)). Touches no device. */
+int bs_validate_segments(const bs_copy_seg* segs, int nseg, int R_src, int W_src, int R_stg, int W_stg, int R_dst,
+                         int W_dst, int src_is_dst, int stg_is_dst);
 
 /*
  * K1 -- gather of the active blocks (paragraph "Vectorized mixed-schedule
@@ -190,7 +205,9 @@ int bs_dual_cache_block_attention(bs_ctx* ctx, const bs_req_desc* reqs, int n, i
  * logits: [n][L] rows of V elements of `logits_dt`, row (i, j) starting at
  * logits + (i * L + j) * logits_row_stride elements (stride >= V, stride *
  * element size a multiple of 16 bytes, base 16-byte aligned). Only rows
- * j in M are read; they must be finite. tokens [n][L] int32 and masked [n][L]
+ * j in M are read; their entries are finite or -inf (a vocabulary entry that
+ * is ruled out), with at least one finite entry per row; NaN and +inf are
+ * outside the contract. tokens [n][L] int32 and masked [n][L]
  * uint8 are updated in place. q_min >= 1 (at least one unmask per step while
  * any position is masked); L <= 64.
  * ws: device workspace of at least bs_decode_workspace_bytes(...) bytes,
@@ -292,6 +309,8 @@ int bs_dual_cache_refresh(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, in
  * unchanged. Rules (BS_ERR_OVERLAP otherwise): destination ranges are
  * pairwise disjoint; when a source box is the destination box (same
  * pointers), no source range of a segment intersects any destination range.
+ * A segment of length 0 copies nothing and takes no part in these rules
+ * (bs_validate_segments applies the same checks on the host alone).
  * D * elem must be a multiple of 16 bytes. stg_* may be NULL when no segment
  * has src_kind 1; src_* may be NULL when none has src_kind 0.
  */

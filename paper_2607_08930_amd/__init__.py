@@ -20,6 +20,7 @@ import numpy as np
 __all__ = [
     "REQ_DTYPE", "SEG_DTYPE", "BS_F32", "BS_BF16", "BlockServeError", "Context", "lib", "LIB_PATH",
     "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
+    "bs_validate_segments",
     "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_gather_active_blocks_n",
     "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_profile_begin", "bs_profile_end",
     "bs_sched_create", "bs_sched_destroy", "bs_sched_submit", "bs_sched_refill", "bs_sched_complete",
@@ -75,6 +76,7 @@ _SIGS = {
     "bs_status_string": (ctypes.c_char_p, [_i32]),
     "bs_last_error": (ctypes.c_char_p, [_vp]),
     "bs_validate_requests": (_i32, [_vp, _i32, _i32, _i32, _i32]),
+    "bs_validate_segments": (_i32, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "bs_gather_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _i32, _vp, _vp, _vp]),
     "bs_scatter_active_blocks": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i64, _vp]),
     "bs_gather_active_blocks_n": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -204,6 +206,13 @@ def bs_last_error(ctx: Context | None = None) -> str:
 def bs_validate_requests(reqs, L: int, R: int, W: int) -> None:
     r = _host(reqs, REQ_DTYPE)
     _check(lib.bs_validate_requests(_ptr(r), len(r), L, R, W))
+
+
+def bs_validate_segments(segs, R_src: int, W_src: int, R_stg: int, W_stg: int, R_dst: int, W_dst: int,
+                         src_is_dst: bool = False, stg_is_dst: bool = False) -> None:
+    g = _host(segs, SEG_DTYPE)
+    _check(lib.bs_validate_segments(_ptr(g) if len(g) else None, len(g), R_src, W_src, R_stg, W_stg, R_dst, W_dst,
+                                    int(bool(src_is_dst)), int(bool(stg_is_dst))))
 
 
 def bs_gather_active_blocks(ctx, reqs, L, R, W, src, src_row_stride_bytes, elem_bytes, dst, pos_out=None,

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -17,7 +18,12 @@ using namespace bs;
 
 namespace {
 
+// Upload slots: the ring starts with kSlots and grows, instead of waiting for
+// the device, while every slot is still read by queued work; only past
+// kMaxSlots distinct descriptor sets in flight does a call wait for the
+// least recently used one.
 constexpr int kSlots = 16;
+constexpr int kMaxSlots = 256;
 
 // An upload slot holds one device blob (descriptors plus the work list derived
 // from them) and the host key it was built from. The key is the small input
@@ -35,6 +41,7 @@ struct Slot {
   hipEvent_t ready = nullptr;  // recorded after the upload
   hipEvent_t done = nullptr;   // recorded after the last launch that read it
   hipStream_t stream = nullptr;
+  uint64_t used = 0;           // tick of the last call that used it (LRU order)
   bool live = false;
 };
 
@@ -61,8 +68,8 @@ struct Prof {
 
 struct bs_ctx {
   int device = 0;
-  Slot slots[kSlots];
-  int next = 0;
+  std::vector<std::unique_ptr<Slot>> slots;   // stable addresses: calls hold Slot*
+  uint64_t tick = 0;
   std::string err;
   Prof prof;
 };
@@ -148,18 +155,63 @@ struct Key {
   }
 };
 
+// Slot for a new blob: a new one while the ring holds fewer than kSlots
+// (that many blobs stay cached); then the least recently used slot that no
+// queued work still reads; a new slot while none is free and the ring is
+// below kMaxSlots; otherwise (more than kMaxSlots descriptor sets in flight)
+// the least recently used slot after waiting for its last reader -- the one
+// bounded host wait.
+int take_slot(bs_ctx* c, Slot** out) {
+  if (c->slots.size() < (size_t)kSlots) {
+    c->slots.push_back(std::make_unique<Slot>());
+    *out = c->slots.back().get();
+    return BS_OK;
+  }
+  Slot* lru_free = nullptr;
+  Slot* lru_any = nullptr;
+  for (auto& p : c->slots) {
+    Slot* sl = p.get();
+    if (!lru_any || sl->used < lru_any->used) lru_any = sl;
+    bool free_ = !sl->live;
+    if (!free_) {
+      const hipError_t q = hipEventQuery(sl->done);
+      if (q == hipSuccess)
+        free_ = true;
+      else if (q != hipErrorNotReady)
+        return hip_fail(c, q, "hipEventQuery(slot)");
+    }
+    if (free_ && (!lru_free || sl->used < lru_free->used)) lru_free = sl;
+  }
+  Slot* sl = lru_free;
+  if (!sl && c->slots.size() < (size_t)kMaxSlots) {
+    c->slots.push_back(std::make_unique<Slot>());
+    sl = c->slots.back().get();
+  }
+  if (!sl) {
+    sl = lru_any;
+    hipError_t e = hipEventSynchronize(sl->done);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize(slot)");
+  }
+  sl->live = false;
+  *out = sl;
+  return BS_OK;
+}
+
 // Find the slot built from `key`, or build the blob with make(Blob&) and
-// upload it into the least recently used slot.
+// upload it into a slot no queued work reads (take_slot).
 template <class Make>
 int upload(bs_ctx* c, hipStream_t s, const Key& key, Make make, Slot** out) {
   const uint64_t hv = fnv1a(key.b.data(), key.b.size());
-  for (Slot& sl : c->slots) {
+  ++c->tick;
+  for (auto& p : c->slots) {
+    Slot& sl = *p;
     if (sl.live && sl.hash == hv && sl.key == key.b) {
       if (sl.stream != s) {
         hipError_t e = hipStreamWaitEvent(s, sl.done, 0);
         if (e != hipSuccess) return hip_fail(c, e, "hipStreamWaitEvent");
         sl.stream = s;
       }
+      sl.used = c->tick;
       *out = &sl;
       return BS_OK;
     }
@@ -167,13 +219,11 @@ int upload(bs_ctx* c, hipStream_t s, const Key& key, Make make, Slot** out) {
   Blob blob;
   make(blob);
   const size_t n = blob.bytes.size();
-  Slot& sl = c->slots[c->next];
-  c->next = (c->next + 1) % kSlots;
-  if (sl.live) {
-    hipError_t e = hipEventSynchronize(sl.done);
-    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize(slot)");
-    sl.live = false;
-  }
+  Slot* slp = nullptr;
+  int st = take_slot(c, &slp);
+  if (st) return st;
+  Slot& sl = *slp;
+  sl.used = c->tick;
   if (sl.cap < n) {
     if (sl.d) (void)hipFree(sl.d);
     if (sl.h) (void)hipHostFree(sl.h);
@@ -388,6 +438,72 @@ DecArgs decode_args(const bs_req_desc* dreqs, int n, int L, int V, bs_dtype logi
   return a;
 }
 
+// ---- K4 segment rules (host only)
+// Every segment has len >= 0, a known source kind, and source and destination
+// ranges inside their boxes. Segments of length 0 copy nothing and take no
+// part in the overlap rules. Destination ranges are pairwise disjoint (a
+// sweep over each row in column order, keeping the furthest end seen so far,
+// so no pair can hide behind another). When a source box is the destination
+// box (src_alias / stg_alias), no source range of that kind meets any
+// destination range.
+int check_segments(bs_ctx* c, const bs_copy_seg* segs, int nseg, int R_src, int W_src, int R_stg, int W_stg,
+                   int R_dst, int W_dst, bool src_alias, bool stg_alias) {
+  if (nseg < 0) return fail(c, BS_ERR_INVALID_ARG, "nseg < 0");
+  if (nseg > 0 && !segs) return fail(c, BS_ERR_INVALID_ARG, "segs is NULL");
+  for (int i = 0; i < nseg; ++i) {
+    const bs_copy_seg& g = segs[i];
+    if (g.len < 0) return fail(c, BS_ERR_INVALID_ARG, "segment %d: len < 0", i);
+    if (g.src_kind != 0 && g.src_kind != 1) return fail(c, BS_ERR_INVALID_ARG, "segment %d: src_kind %d", i, g.src_kind);
+    const int Rs = g.src_kind ? R_stg : R_src, Ws = g.src_kind ? W_stg : W_src;
+    if (g.src_row < 0 || g.src_row >= Rs || g.src_col < 0 || (int64_t)g.src_col + g.len > Ws)
+      return fail(c, BS_ERR_INVALID_ARG, "segment %d: source range outside its box", i);
+    if (g.dst_row < 0 || g.dst_row >= R_dst || g.dst_col < 0 || (int64_t)g.dst_col + g.len > W_dst)
+      return fail(c, BS_ERR_INVALID_ARG, "segment %d: destination range outside the box", i);
+  }
+  std::vector<int> order;
+  order.reserve((size_t)nseg);
+  for (int i = 0; i < nseg; ++i)
+    if (segs[i].len > 0) order.push_back(i);
+  std::sort(order.begin(), order.end(), [&](int x, int y) {
+    return segs[x].dst_row != segs[y].dst_row ? segs[x].dst_row < segs[y].dst_row : segs[x].dst_col < segs[y].dst_col;
+  });
+  int64_t reach = 0;   // furthest destination end so far in the current row
+  int reach_seg = -1;
+  for (size_t t = 0; t < order.size(); ++t) {
+    const bs_copy_seg& y = segs[order[t]];
+    if (t == 0 || segs[order[t - 1]].dst_row != y.dst_row) {
+      reach = 0;
+      reach_seg = -1;
+    }
+    if (reach_seg >= 0 && reach > y.dst_col)
+      return fail(c, BS_ERR_OVERLAP, "segments %d and %d write overlapping destination cells", reach_seg, order[t]);
+    if ((int64_t)y.dst_col + y.len > reach) {
+      reach = (int64_t)y.dst_col + y.len;
+      reach_seg = order[t];
+    }
+  }
+  if (src_alias || stg_alias) {
+    // destinations are now known disjoint and sorted: for a source range
+    // [a, b) on row r only the last destination of row r starting before b
+    // can meet it
+    for (int i = 0; i < nseg; ++i) {
+      const bs_copy_seg& g = segs[i];
+      if (g.len == 0 || (g.src_kind == 0 && !src_alias) || (g.src_kind == 1 && !stg_alias)) continue;
+      const int64_t a = g.src_col, b = (int64_t)g.src_col + g.len;
+      auto it = std::lower_bound(order.begin(), order.end(), 0, [&](int x, int) {
+        const bs_copy_seg& d = segs[x];
+        return d.dst_row < g.src_row || (d.dst_row == g.src_row && d.dst_col < b);
+      });
+      if (it == order.begin()) continue;
+      const int jj = *(it - 1);
+      const bs_copy_seg& d = segs[jj];
+      if (d.dst_row == g.src_row && (int64_t)d.dst_col + d.len > a)
+        return fail(c, BS_ERR_OVERLAP, "segment %d reads cells that segment %d writes", i, jj);
+    }
+  }
+  return BS_OK;
+}
+
 // ---- phase timing of the fused step
 hipError_t prof_mark(bs_ctx* c, int phase, hipStream_t s) {
   Prof& p = c->prof;
@@ -416,7 +532,8 @@ int bs_destroy(bs_ctx* c) {
   if (!c) return BS_OK;
   DeviceGuard dg(c->device);
   for (hipEvent_t e : c->prof.ev) (void)hipEventDestroy(e);
-  for (Slot& sl : c->slots) {
+  for (auto& p : c->slots) {
+    Slot& sl = *p;
     if (sl.live) (void)hipEventSynchronize(sl.done);
     if (sl.d) (void)hipFree(sl.d);
     if (sl.h) (void)hipHostFree(sl.h);
@@ -444,6 +561,12 @@ const char* bs_last_error(const bs_ctx* c) { return c ? c->err.c_str() : g_err.c
 
 int bs_validate_requests(const bs_req_desc* reqs, int n, int L, int R, int W) {
   return check_reqs(nullptr, reqs, n, L, R, W);
+}
+
+int bs_validate_segments(const bs_copy_seg* segs, int nseg, int R_src, int W_src, int R_stg, int W_stg, int R_dst,
+                         int W_dst, int src_is_dst, int stg_is_dst) {
+  return check_segments(nullptr, segs, nseg, R_src, W_src, R_stg, W_stg, R_dst, W_dst, src_is_dst != 0,
+                        stg_is_dst != 0);
 }
 
 // ------------------------------------------------------------------ K1
@@ -857,19 +980,13 @@ int bs_kv_scatter_compact(bs_ctx* c, const bs_copy_seg* segs, int nseg, int n_la
   const int64_t row_bytes = (int64_t)D * eb;
   if (row_bytes % 16) return fail(c, BS_ERR_UNSUPPORTED, "D*elem=%lld not a multiple of 16 bytes", (long long)row_bytes);
   bool any_src = false, any_stg = false;
+  for (int i = 0; i < nseg; ++i) (segs[i].src_kind ? any_stg : any_src) = true;
+  const bool src_alias = any_src && (src_k == dst_k || src_v == dst_v || src_k == dst_v || src_v == dst_k);
+  const bool stg_alias = any_stg && (stg_k == dst_k || stg_v == dst_v || stg_k == dst_v || stg_v == dst_k);
+  int st = check_segments(c, segs, nseg, R_src, W_src, R_stg, W_stg, R_dst, W_dst, src_alias, stg_alias);
+  if (st) return st;
   int64_t total_chunks = 0;
-  for (int i = 0; i < nseg; ++i) {
-    const bs_copy_seg& g = segs[i];
-    if (g.len < 0) return fail(c, BS_ERR_INVALID_ARG, "segment %d: len < 0", i);
-    if (g.src_kind != 0 && g.src_kind != 1) return fail(c, BS_ERR_INVALID_ARG, "segment %d: src_kind %d", i, g.src_kind);
-    const int Rs = g.src_kind ? R_stg : R_src, Ws = g.src_kind ? W_stg : W_src;
-    if (g.src_kind) any_stg = true; else any_src = true;
-    if (g.src_row < 0 || g.src_row >= Rs || g.src_col < 0 || (int64_t)g.src_col + g.len > Ws)
-      return fail(c, BS_ERR_INVALID_ARG, "segment %d: source range outside its box", i);
-    if (g.dst_row < 0 || g.dst_row >= R_dst || g.dst_col < 0 || (int64_t)g.dst_col + g.len > W_dst)
-      return fail(c, BS_ERR_INVALID_ARG, "segment %d: destination range outside the box", i);
-    total_chunks += (g.len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
-  }
+  for (int i = 0; i < nseg; ++i) total_chunks += (segs[i].len * row_bytes + kCopyChunkBytes - 1) / kCopyChunkBytes;
   if (any_src && (!src_k || !src_v)) return fail(c, BS_ERR_INVALID_ARG, "src box is NULL");
   if (any_stg && (!stg_k || !stg_v)) return fail(c, BS_ERR_INVALID_ARG, "staging box is NULL");
   if (nseg > 0 && (!dst_k || !dst_v)) return fail(c, BS_ERR_INVALID_ARG, "dst box is NULL");
@@ -879,37 +996,12 @@ int bs_kv_scatter_compact(bs_ctx* c, const bs_copy_seg* segs, int nseg, int n_la
     return fail(c, BS_ERR_INVALID_ARG, "layer stride smaller than one box or not a multiple of 16 bytes");
   for (const void* p : {src_k, src_v, stg_k, stg_v, (const void*)dst_k, (const void*)dst_v})
     if (p && !aligned(p, 16)) return fail(c, BS_ERR_INVALID_ARG, "box pointers must be 16-byte aligned");
-  // destinations pairwise disjoint; no source range of an aliased box meets a destination
-  std::vector<int> order(nseg);
-  for (int i = 0; i < nseg; ++i) order[i] = i;
-  std::sort(order.begin(), order.end(), [&](int x, int y) {
-    return segs[x].dst_row != segs[y].dst_row ? segs[x].dst_row < segs[y].dst_row : segs[x].dst_col < segs[y].dst_col;
-  });
-  for (int t = 1; t < nseg; ++t) {
-    const bs_copy_seg &x = segs[order[t - 1]], &y = segs[order[t]];
-    if (x.len > 0 && y.len > 0 && x.dst_row == y.dst_row && (int64_t)x.dst_col + x.len > y.dst_col)
-      return fail(c, BS_ERR_OVERLAP, "segments %d and %d write overlapping destination cells", order[t - 1], order[t]);
-  }
-  const bool src_alias = any_src && (src_k == dst_k || src_v == dst_v || src_k == dst_v || src_v == dst_k);
-  const bool stg_alias = any_stg && (stg_k == dst_k || stg_v == dst_v || stg_k == dst_v || stg_v == dst_k);
-  if (src_alias || stg_alias) {
-    for (int i = 0; i < nseg; ++i) {
-      const bs_copy_seg& g = segs[i];
-      if (g.len == 0 || (g.src_kind == 0 && !src_alias) || (g.src_kind == 1 && !stg_alias)) continue;
-      for (int jj = 0; jj < nseg; ++jj) {
-        const bs_copy_seg& d = segs[jj];
-        if (d.len == 0 || d.dst_row != g.src_row) continue;
-        if (g.src_col < d.dst_col + d.len && d.dst_col < g.src_col + g.len)
-          return fail(c, BS_ERR_OVERLAP, "segment %d reads cells that segment %d writes", i, jj);
-      }
-    }
-  }
   if (nseg == 0 || n_layers == 0 || total_chunks == 0) return BS_OK;
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  int st = upload(c, s, Key('C', {nseg, row_bytes}, segs, sizeof(bs_copy_seg) * nseg), [&](Blob& blob) {
+  st = upload(c, s, Key('C', {nseg, row_bytes}, segs, sizeof(bs_copy_seg) * nseg), [&](Blob& blob) {
     std::vector<CopyUnit> units;
     units.reserve((size_t)total_chunks);
     for (int i = 0; i < nseg; ++i) {

@@ -108,3 +108,75 @@ def test_package_has_no_cpu_fallback():
     src = inspect.getsource(bs)
     assert "oracle" not in src.replace("oracle/", "")
     assert "import synth" not in src
+
+
+def segs_of(rows):
+    return np.array(rows, bs.SEG_DTYPE)
+
+
+def test_validate_segments_zero_length_cannot_hide_an_overlap():
+    # A = [0, 10) and C = [5, 6) on one destination row, with a zero-length
+    # Z = [3, 3) that sorts between them
+    a, z, c = (1, 0, 0, 2, 0, 10), (1, 1, 0, 2, 3, 0), (1, 2, 0, 2, 5, 1)
+    for order in ([a, z, c], [z, a, c], [c, z, a], [a, c, z]):
+        with pytest.raises(bs.BlockServeError, match="overlapping") as e:
+            bs.bs_validate_segments(segs_of(order), 4, 16, 4, 16, 4, 16)
+        assert e.value.name == "BS_ERR_OVERLAP"
+    # a long range covering a later one past an intermediate disjoint one
+    with pytest.raises(bs.BlockServeError, match="overlapping"):
+        bs.bs_validate_segments(segs_of([(1, 0, 0, 0, 0, 12), (1, 1, 0, 0, 2, 1), (1, 2, 0, 0, 9, 2)]),
+                                4, 16, 4, 16, 4, 16)
+    # zero-length segments alone never overlap, even at a covered cell
+    bs.bs_validate_segments(segs_of([(1, 0, 0, 2, 0, 10), (1, 1, 0, 2, 3, 0), (1, 2, 0, 2, 10, 4)]),
+                            4, 16, 4, 16, 4, 16)
+    bs.bs_validate_segments(segs_of([]), 4, 16, 4, 16, 4, 16)
+
+
+def test_validate_segments_rules():
+    ok = [(0, 0, 0, 1, 0, 8), (1, 0, 0, 0, 8, 8), (0, 3, 2, 3, 0, 4)]
+    bs.bs_validate_segments(segs_of(ok), 4, 16, 2, 16, 4, 16)
+    for bad, msg in [((0, 4, 0, 0, 0, 1), "source range"), ((1, 2, 0, 0, 0, 1), "source range"),
+                     ((0, 0, 10, 0, 0, 7), "source range"), ((0, 0, 0, 0, 12, 5), "destination range"),
+                     ((0, 0, 0, -1, 0, 1), "destination range"), ((2, 0, 0, 0, 0, 1), "src_kind"),
+                     ((0, 0, 0, 0, 0, -1), "len < 0")]:
+        with pytest.raises(bs.BlockServeError, match=msg) as e:
+            bs.bs_validate_segments(segs_of([bad]), 4, 16, 2, 16, 4, 16)
+        assert e.value.name == "BS_ERR_INVALID_ARG"
+    # in place: a source range that another segment writes is rejected only
+    # when the source box is the destination box
+    alias = [(0, 1, 0, 2, 0, 4), (0, 3, 0, 1, 2, 4)]          # reads row 1 [0, 4), writes row 1 [2, 6)
+    bs.bs_validate_segments(segs_of(alias), 4, 16, 2, 16, 4, 16)
+    with pytest.raises(bs.BlockServeError, match="reads cells") as e:
+        bs.bs_validate_segments(segs_of(alias), 4, 16, 2, 16, 4, 16, src_is_dst=True)
+    assert e.value.name == "BS_ERR_OVERLAP"
+    # touching ranges are disjoint; staging aliasing is checked for kind 1 only
+    bs.bs_validate_segments(segs_of([(0, 1, 0, 2, 0, 4), (0, 3, 0, 1, 4, 4)]), 4, 16, 2, 16, 4, 16,
+                            src_is_dst=True)
+    bs.bs_validate_segments(segs_of(alias), 4, 16, 2, 16, 4, 16, stg_is_dst=True)
+
+
+def test_validate_segments_against_brute_force():
+    # random segment sets: the library's verdict equals a cell-by-cell check
+    rng = np.random.default_rng(7)
+    for trial in range(400):
+        n = int(rng.integers(1, 7))
+        rows = [(int(rng.integers(0, 2)), int(rng.integers(0, 3)), int(rng.integers(0, 8)),
+                 int(rng.integers(0, 3)), int(rng.integers(0, 12)), int(rng.integers(0, 5))) for _ in range(n)]
+        rows = [(k, r, min(c, 16 - ln), dr, min(dc, 16 - ln), ln) for k, r, c, dr, dc, ln in rows]
+        in_place = bool(trial % 2)
+        owner = {}
+        expect = None
+        for i, (k, r, c, dr, dc, ln) in enumerate(rows):
+            for t in range(ln):
+                if (dr, dc + t) in owner:
+                    expect = "overlapping"
+                owner[(dr, dc + t)] = i
+        if expect is None and in_place:
+            for k, r, c, dr, dc, ln in rows:
+                if k == 0 and any((r, c + t) in owner for t in range(ln)):
+                    expect = "reads cells"
+        if expect is None:
+            bs.bs_validate_segments(segs_of(rows), 3, 16, 3, 16, 3, 16, src_is_dst=in_place)
+        else:
+            with pytest.raises(bs.BlockServeError, match=expect):
+                bs.bs_validate_segments(segs_of(rows), 3, 16, 3, 16, 3, 16, src_is_dst=in_place)

@@ -174,17 +174,19 @@ __device__ inline void select_request(const DecArgs& a, int i, int lane) {
 #pragma unroll
     for (int p = 0; p < kUnroll; ++p) M = fmaxf(M, pr[p].m);   // repeats of the last part change nothing
     for (int p = kUnroll; p < a.parts; ++p) M = fmaxf(M, pp[p].m);
+    // parts without a finite logit (m = -inf, s = 0) add nothing; they are
+    // skipped so that (-inf) - M never reaches the exponential
     float S = 0.0f;
     int A = INT_MAX;
 #pragma unroll
     for (int p = 0; p < kUnroll; ++p)
       if (p < a.parts) {
-        S += pr[p].s * __builtin_amdgcn_exp2f((pr[p].m - M) * kLog2e);
+        if (pr[p].m != -__builtin_inff()) S += pr[p].s * __builtin_amdgcn_exp2f((pr[p].m - M) * kLog2e);
         if (pr[p].m == M) A = min(A, pr[p].a);
       }
     for (int p = kUnroll; p < a.parts; ++p) {
       const DecPartial x = pp[p];
-      S += x.s * __builtin_amdgcn_exp2f((x.m - M) * kLog2e);
+      if (x.m != -__builtin_inff()) S += x.s * __builtin_amdgcn_exp2f((x.m - M) * kLog2e);
       if (x.m == M) A = min(A, x.a);
     }
     conf = 1.0f / S;
@@ -273,8 +275,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   float M = sm[0];
 #pragma unroll
   for (int k = 1; k < kThreads / 64; ++k) M = vmax(M, sm[k]);
-  // r.mb <= r.mt * log2 e <= M * log2 e, so the factor is at most 1
-  const float sc = r.s * __builtin_amdgcn_exp2f(r.mb - M * kLog2e);
+  // r.mb <= r.mt * log2 e <= M * log2 e, so the factor is at most 1. A part
+  // whose logits are all -inf (M = -inf) sums to 0: its threads hold s = 0
+  // and mb = -FLT_MAX, and exp2(mb - M) would be exp2(+inf).
+  const float sc = M == -__builtin_inff() ? 0.0f : r.s * __builtin_amdgcn_exp2f(r.mb - M * kLog2e);
   // smallest index holding M: threads whose max is M re-read the one vector
   // where they first saw it
   int arg = INT_MAX;

@@ -113,45 +113,156 @@ def run_decode(ctx, w, logits, tok_c, msk_c, *, tau=None, q_min=None, eos_id=Non
                 done=done.cpu().numpy(), eos_seen=eos.cpu().numpy(), conf=conf.cpu().numpy(), ws=ws)
 
 
-def exempt_requests(ref, reqs, L, tau, q_min=1):
-    """Requests whose selection is not fixed at fp32 precision: the number
-    selected changes when every confidence within EXEMPT of tau moves by
-    EXEMPT either way, or the last selected and first unselected confidences
-    are within EXEMPT of each other. (A confidence near tau that cannot change
-    the count -- e.g. when the quota q_min decides it -- exempts nothing.)"""
-    ex = set()
-    for i, r in enumerate(reqs):
-        t = oracle.geometry(r, L)
-        cs = sorted((ref["conf"][i, j] for j in range(t.B) if ref["conf"][i, j] >= 0), reverse=True)
-        if not cs:
-            continue
-        nm = len(cs)
-        n_lo = min(nm, max(q_min, sum(c >= tau + EXEMPT for c in cs)))
-        n_hi = min(nm, max(q_min, sum(c >= tau - EXEMPT for c in cs)))
-        nsel = int(ref["n_unmasked"][i])
-        if n_lo != n_hi:
-            ex.add(i)
-        elif 0 < nsel < nm and cs[nsel - 1] - cs[nsel] <= EXEMPT:
-            ex.add(i)
-    return ex
+class DecodeStats:
+    """Counts of one decode comparison: masked positions compared, positions
+    exempt because a confidence lies within EXEMPT of tau or of a
+    neighbour at the selection boundary (the band), positions whose argmax
+    is not fixed by the arithmetic (near ties, output head only), and
+    requests whose selection count the band leaves open."""
+
+    def __init__(self):
+        self.positions = 0
+        self.band = 0
+        self.near_tie = 0
+        self.open_requests = 0
+
+    def add(self, o):
+        for k in ("positions", "band", "near_tie", "open_requests"):
+            setattr(self, k, getattr(self, k) + getattr(o, k))
+        return self
+
+    def __repr__(self):
+        return (f"{self.positions} masked positions, {self.band} in the threshold/tie band, "
+                f"{self.near_tie} near argmax ties, {self.open_requests} requests with an open count")
 
 
-def check_decode(w, got, ref, reqs=None, tau=None, label="", q_min=None, conf_tol=CONF_TOL, also_exempt=()):
+def selection_bands(conf_row, M, tau, q_min, eps=EXEMPT):
+    """Per masked position j of one request: 'sel' when the decision rule
+    selects j for every set of confidences within eps of conf_row, 'not' when
+    it never does, 'band' otherwise; and the bounds (n_lo, n_hi) of the
+    selection count over that set.
+
+    The rule selects the n = min(|M|, max(q, #{c >= tau})) most confident
+    positions (ties to the smaller j). Moving every confidence by at most eps
+    keeps n in [n_lo, n_hi] (counts at tau + eps and tau - eps); at most
+    #{k != j : c_k >= c_j - eps} positions can then rank ahead of j and at
+    least #{k != j : c_k > c_j + eps} do."""
+    c = np.array([conf_row[j] for j in M], np.float64)
+    nm = len(M)
+    n_lo = min(nm, max(q_min, int((c >= tau + eps).sum())))
+    n_hi = min(nm, max(q_min, int((c >= tau - eps).sum())))
+    status = {}
+    for a, j in enumerate(M):
+        others = np.delete(c, a)
+        ahead_max = int((others >= c[a] - eps).sum())
+        ahead_min = int((others > c[a] + eps).sum())
+        status[j] = "sel" if ahead_max < n_lo else ("not" if ahead_min >= n_hi else "band")
+    return status, n_lo, n_hi
+
+
+def check_request_decode(label, i, B, tok_in, msk_in, got_tok, got_msk, got_conf, got_n, got_done, got_eos,
+                         ref_conf, ref_pred, tau, q_min, eos_id, conf_tol, alt_ids=None):
+    """One request's decode against the oracle, position by position.
+
+    * confidences: computed exactly where the oracle computes them, within
+      conf_tol; -1 elsewhere;
+    * a position the rule decides the same way for every confidence within
+      EXEMPT of the oracle's ('sel' / 'not') must be unmasked with the
+      oracle's argmax, or left masked with its token unchanged; a 'band'
+      position may do either (counted);
+    * near argmax ties (alt_ids[j]: every id whose logit is within the tie
+      gap of the largest) may take any of those ids (counted);
+    * the GPU's own result must obey the rule on the GPU's own confidences:
+      n = min(|M|, max(q, #{c >= tau})) positions, the n most confident
+      (ties to the smaller j); and n_unmasked, done, eos_seen must describe
+      its own tokens and mask;
+    * positions outside M are untouched.
+    Returns DecodeStats."""
+    st = DecodeStats()
+    alt_ids = alt_ids or {}
+    M = [j for j in range(B) if msk_in[j]]
+    assert CONF_TOL <= conf_tol < EXEMPT / 2, "the band argument needs conf_tol well below EXEMPT"
+    for j in range(len(got_conf)):
+        if j in M:
+            assert ref_conf[j] >= 0, f"{label}: oracle lacks confidence at ({i},{j})"
+            assert abs(float(got_conf[j]) - ref_conf[j]) <= conf_tol, \
+                f"{label}: confidence error {abs(float(got_conf[j]) - ref_conf[j]):.2e} at ({i},{j})"
+        else:
+            assert got_conf[j] == -1, f"{label}: conf_out not -1 at unmasked ({i},{j})"
+    for j in range(B, len(tok_in)):
+        assert got_tok[j] == tok_in[j] and got_msk[j] == msk_in[j], f"{label}: cell past the block changed ({i},{j})"
+    for j in range(B):
+        if j not in M:
+            assert got_tok[j] == tok_in[j] and got_msk[j] == msk_in[j], f"{label}: unmasked cell changed ({i},{j})"
+    if not M:
+        assert got_n == 0 and got_done == 1, f"{label}: empty request {i} not a no-op"
+    else:
+        status, n_lo, n_hi = selection_bands(ref_conf, M, tau, q_min)
+        st.positions = len(M)
+        st.open_requests = int(n_lo != n_hi)
+        for j in M:
+            ok_ids = alt_ids.get(j, {int(ref_pred[j])})
+            if len(ok_ids) > 1:
+                st.near_tie += 1
+            if got_msk[j] == 0:
+                assert int(got_tok[j]) in ok_ids, \
+                    f"{label}: ({i},{j}) unmasked with {int(got_tok[j])}, oracle argmax {int(ref_pred[j])}"
+                assert status[j] != "not", f"{label}: ({i},{j}) unmasked, the rule never selects it"
+            else:
+                assert got_msk[j] == 1 and got_tok[j] == tok_in[j], f"{label}: ({i},{j}) masked cell changed"
+                assert status[j] != "sel", f"{label}: ({i},{j}) left masked, the rule always selects it"
+            st.band += status[j] == "band"
+        # the GPU's decision obeys the rule on its own confidences
+        g = np.array([float(got_conf[j]) for j in M], np.float32)
+        n_gpu = min(len(M), max(q_min, int((g >= np.float32(tau)).sum())))
+        order = sorted(range(len(M)), key=lambda a: (-g[a], M[a]))
+        chosen = {M[a] for a in order[:n_gpu]}
+        unmasked = {j for j in M if got_msk[j] == 0}
+        assert unmasked == chosen, f"{label}: request {i} selected {sorted(unmasked)}, its own rule {sorted(chosen)}"
+        assert got_n == n_gpu and n_lo <= n_gpu <= n_hi, f"{label}: request {i} n_unmasked {got_n} ({n_lo}..{n_hi})"
+        assert got_done == int(n_gpu == len(M)), f"{label}: request {i} done flag"
+    eos = eos_id >= 0 and any(got_msk[j] == 0 and got_tok[j] == eos_id for j in range(B))
+    assert got_eos == int(eos), f"{label}: request {i} eos_seen"
+    return st
+
+
+def check_decode(w, got, ref, reqs=None, tau=None, label="", q_min=None, conf_tol=CONF_TOL, alt_ids=None,
+                 tok_in=None, msk_in=None, eos_id=None):
+    """Compact-state decode results against the oracle's, per position (see
+    check_request_decode). tok_in / msk_in: the compact state before the call
+    (default: recovered from the oracle's result and its selections).
+    alt_ids: {(i, j): ids} near argmax ties. Returns DecodeStats."""
     reqs = w.reqs if reqs is None else reqs
     tau = w.tau if tau is None else tau
-    ex = exempt_requests(ref, reqs, w.L, tau, w.q_min if q_min is None else q_min) | set(also_exempt)
+    q_min = w.q_min if q_min is None else q_min
+    eos_id = w.eos_id if eos_id is None else eos_id
+    if msk_in is None:
+        msk_in = (ref["masked"].astype(bool) | (ref["conf"] >= 0)).astype(np.uint8)
+    if tok_in is None:
+        raise ValueError("check_decode needs the input tokens")
+    stats = DecodeStats()
     for i, r in enumerate(reqs):
-        t = oracle.geometry(r, w.L)
-        m = ref["conf"][i] >= 0
-        assert np.array_equal(got["conf"][i] >= 0, m), f"{label}: conf_out mask differs (request {i})"
-        if m.any():
-            dc = np.abs(got["conf"][i][m] - ref["conf"][i][m]).max()
-            assert dc <= conf_tol, f"{label}: confidence error {dc:.2e} (request {i})"
-        assert (got["conf"][i][~m] == -1).all()
-        if i in ex:
-            continue
-        assert np.array_equal(got["tokens"][i], ref["tokens"][i]), f"{label}: tokens differ (request {i})"
-        assert np.array_equal(got["masked"][i], ref["masked"][i]), f"{label}: mask differs (request {i})"
-        for key in ("n_unmasked", "done", "eos_seen"):
-            assert got[key][i] == ref[key][i], f"{label}: {key} differs (request {i})"
-    return len(ex)
+        B = oracle.geometry(r, w.L).B
+        alt = {j: ids for (ii, j), ids in (alt_ids or {}).items() if ii == i}
+        stats.add(check_request_decode(label, i, B, tok_in[i], msk_in[i], got["tokens"][i], got["masked"][i],
+                                       got["conf"][i], int(got["n_unmasked"][i]), int(got["done"][i]),
+                                       int(got["eos_seen"][i]), ref["conf"][i], ref["pred"][i], tau, q_min,
+                                       eos_id, conf_tol, alt))
+    return stats
+
+
+def check_step_decode(w, reqs, got, dec, tok_in, msk_in, label, only=None):
+    """The fused step's decode, per position, on the dense boxes: each
+    request's block cells are gathered from the result and from the input
+    state and compared with the oracle's decode (check_request_decode)."""
+    gtok, _ = oracle.gather_active_blocks(reqs, w.L, got["tokens"])
+    gmsk, _ = oracle.gather_active_blocks(reqs, w.L, got["mask"])
+    itok, _ = oracle.gather_active_blocks(reqs, w.L, tok_in)
+    imsk, _ = oracle.gather_active_blocks(reqs, w.L, msk_in)
+    stats = DecodeStats()
+    for i in (range(len(reqs)) if only is None else only):
+        B = oracle.geometry(reqs[i], w.L).B
+        stats.add(check_request_decode(label, i, B, itok[i], imsk[i], gtok[i], gmsk[i], got["conf"][i],
+                                       int(got["n_unmasked"][i]), int(got["done"][i]), int(got["eos_seen"][i]),
+                                       dec["conf"][i], dec["pred"][i], w.tau, w.q_min, w.eos_id, 2e-5))
+    return stats

@@ -8,7 +8,9 @@ The logits are fp32 sums of exact bf16 products on the GPU and exact fp64
 sums in the oracle, so they differ by accumulation rounding (about 1e-5 on
 logits of magnitude 20): confidences agree within LM_CONF_TOL, and a
 position whose two largest oracle logits lie within ARG_GAP may pick either
-id (its request is exempt from the bit-exact token check)."""
+id (that position accepts either id; counted). Selection decisions are
+compared per position, with the 1e-3 band around tau and around ties exempt
+and counted."""
 import numpy as np
 import pytest
 
@@ -59,14 +61,21 @@ def run_lm(ctx, w, hidden, wv, tok_c, msk_c, tau=None, q_min=None, ldw=None, dev
 
 
 def near_ties(w, hidden, wv, msk_c, reqs_idx):
-    """Requests with a masked position whose two largest oracle logits are
-    within ARG_GAP (their predicted id is not fixed at fp32 accumulation)."""
-    keys = [(i, j) for i in reqs_idx for j in range(oracle.geometry(w.reqs[i], w.L).B) if msk_c[i, j]]
+    """{(a, j): ids} for masked positions whose largest oracle logits lie
+    within ARG_GAP of each other (their predicted id is not fixed at fp32
+    accumulation): every id within ARG_GAP of the largest logit is accepted
+    there. a indexes reqs_idx."""
+    keys = [(a, i, j) for a, i in enumerate(reqs_idx) for j in range(oracle.geometry(w.reqs[i], w.L).B)
+            if msk_c[i, j]]
     if not keys:
-        return set()
-    lg = oracle.lm_head_logits(np.stack([hidden[i, j] for i, j in keys]), wv, "bf16")
-    top2 = np.sort(lg, axis=1)[:, -2:] if lg.shape[1] > 1 else np.concatenate([lg, lg - 1e9], 1)
-    return {keys[a][0] for a in range(len(keys)) if top2[a, 1] - top2[a, 0] <= ARG_GAP}
+        return {}
+    lg = oracle.lm_head_logits(np.stack([hidden[i, j] for _, i, j in keys]), wv, "bf16")
+    out = {}
+    for r, (a, i, j) in enumerate(keys):
+        ids = np.nonzero(lg[r] >= lg[r].max() - ARG_GAP)[0]
+        if len(ids) > 1:
+            out[(a, j)] = set(int(v) for v in ids)
+    return out
 
 
 def lm_case(ctx, w, d, label, sample=None, tau=None, q_min=None, ldw=None):
@@ -84,26 +93,28 @@ def lm_case(ctx, w, d, label, sample=None, tau=None, q_min=None, ldw=None):
     ties = near_ties(w, hidden, wv, msk_c, idx)
     sub = {k: v[idx] for k, v in ref.items() if isinstance(v, np.ndarray) and len(v) == w.n}
     gsub = {k: v[idx] for k, v in got.items()}
-    ties_local = {a for a, i in enumerate(idx) if i in ties}
-    nex = check_decode(w, gsub, sub, reqs=w.reqs[idx], tau=tau, label=label, q_min=q_min,
-                       conf_tol=LM_CONF_TOL, also_exempt=ties_local)
-    say(f"  exempt requests: {nex} of {len(idx)} (near ties {len(ties_local)})")
-    # requests outside the sample keep untouched rows beyond their block
-    return got, ref, nex, (hidden, wv, tok_c, msk_c)
+    stats = check_decode(w, gsub, sub, reqs=w.reqs[idx], tau=tau, label=label, q_min=q_min,
+                         conf_tol=LM_CONF_TOL, alt_ids=ties, tok_in=tok_c[idx], msk_in=msk_c[idx])
+    say(f"  {stats}")
+    return got, ref, stats, (hidden, wv, tok_c, msk_c)
+
+
+def band_ok(stats):
+    return stats.band + stats.near_tie <= max(2, stats.positions // 50)
 
 
 def test_lm_head_small_ragged(ctx):
     # V = 1000 (last 256-tile ragged), d = 64 (two K slices), partial blocks, empty prompt
     w = synth.custom(8, 2, 2, 16, 1000, "bf16", [5, 0, 9, 3, 14], [16, 5, 24, 20, 8], [1, 0, 1, 2, 0], W=40)
-    _, _, nex, _ = lm_case(ctx, w, 64, "small")
-    assert nex <= 1
+    _, _, stats, _ = lm_case(ctx, w, 64, "small")
+    assert band_ok(stats), stats
 
 
 @pytest.mark.parametrize("V,d", [(257, 32), (32017, 4096)])
 def test_lm_head_medium(ctx, V, d):
     w = synth.custom(32, 2, 2, 16, V, "bf16", list(range(3, 131, 16)), [64] * 8, [0, 1, 0, 1, 1, 0, 1, 0])
-    _, _, nex, _ = lm_case(ctx, w, d, f"V={V} d={d}")
-    assert nex <= 2
+    _, _, stats, _ = lm_case(ctx, w, d, f"V={V} d={d}")
+    assert band_ok(stats), stats
 
 
 @pytest.mark.parametrize("n", [22, 60, 90])
@@ -111,8 +122,8 @@ def test_lm_head_row_tile_orders(ctx, n):
     # 2, 4 and 6 row tiles of 256 masked rows: the one-row-tile-per-XCD order
     # and the order that keeps all row tiles of a vocabulary tile together
     w = synth.custom(32, 2, 2, 16, 777, "bf16", [5 + 3 * i for i in range(n)], [64] * n, [i % 2 for i in range(n)])
-    _, _, nex, _ = lm_case(ctx, w, 64, f"n={n} rows")
-    assert nex <= n // 8
+    _, _, stats, _ = lm_case(ctx, w, 64, f"n={n} rows")
+    assert band_ok(stats), stats
 
 
 def test_lm_head_largest_row_count(ctx):
@@ -122,8 +133,8 @@ def test_lm_head_largest_row_count(ctx):
     n = 1024
     w = synth.custom(64, 2, 2, 16, 300, "bf16", [3 + i % 17 for i in range(n)], [64] * n, [0] * n)
     sample = sorted(np.random.default_rng(9).choice(n, size=64, replace=False).tolist())
-    _, _, nex, _ = lm_case(ctx, w, 32, "n*L=65536", sample=sample)
-    assert nex <= len(sample) // 8
+    _, _, stats, _ = lm_case(ctx, w, 32, "n*L=65536", sample=sample)
+    assert band_ok(stats), stats
 
 
 @pytest.mark.parametrize("cfg", [2, 3])
@@ -131,8 +142,8 @@ def test_lm_head_full_size_sampled(ctx, cfg):
     w = synth.workload(cfg)
     d = synth.LM_HEAD_DIM[cfg]
     sample = sorted(np.random.default_rng(70 + cfg).choice(w.n, size=6, replace=False).tolist())
-    _, _, nex, _ = lm_case(ctx, w, d, f"cfg{cfg}", sample=sample)
-    assert nex <= 2
+    _, _, stats, _ = lm_case(ctx, w, d, f"cfg{cfg}", sample=sample)
+    assert band_ok(stats), stats
 
 
 def test_lm_head_strided_head_and_quota(ctx):

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import CONF_TOL, check_attention, exempt_requests, lazy, say
+from gpu_util import check_attention, check_step_decode, lazy, say
 
 pytestmark = pytest.mark.gpu
 
@@ -52,34 +52,21 @@ def snapshot(st):
 
 
 def check_step(w, got, ref, host, label):
-    """Attention per layer within tolerance, caches bit-exact, dense state
-    bit-exact outside the exemption set, rows of no request untouched."""
+    """Attention per layer within tolerance, caches bit-exact, decode per
+    position on the dense state (outside the 1e-3 band: bit-exact), cells of
+    the dense boxes outside the active blocks untouched."""
     for l, (g, r) in enumerate(zip(got["layers"], ref["layers"])):
         check_attention(w, g["out"], r["out"], label=f"{label} layer {l}")
         np.testing.assert_array_equal(g["k_cache"], r["k_cache"])     # bf16: bit patterns on both sides
         np.testing.assert_array_equal(g["v_cache"], r["v_cache"])
-    dec = ref["decode"]
-    ex = exempt_requests(dec, w.reqs, w.L, w.tau, w.q_min)
     np.testing.assert_array_equal(got["pos"], ref["pos"])
-    used = set()
-    for i, r in enumerate(w.reqs):
-        used.add(int(r["row"]))
-        m = dec["conf"][i] >= 0
-        assert np.array_equal(got["conf"][i] >= 0, m), f"{label}: conf mask differs (request {i})"
-        if m.any():
-            assert np.abs(got["conf"][i][m] - dec["conf"][i][m]).max() <= CONF_TOL
-        if i in ex:
-            continue
-        row = int(r["row"])
-        assert np.array_equal(got["tokens"][row], ref["tokens"][row]), f"{label}: tokens differ (request {i})"
-        assert np.array_equal(got["mask"][row], ref["mask"][row]), f"{label}: mask differs (request {i})"
-        for key in ("n_unmasked", "done", "eos_seen"):
-            assert got[key][i] == dec[key][i], f"{label}: {key} differs (request {i})"
-    for row in range(w.R):
-        if row not in used:
-            np.testing.assert_array_equal(got["tokens"][row], host["tokens"][row])
-            np.testing.assert_array_equal(got["mask"][row], host["mask"][row])
-    return len(ex)
+    stats = check_step_decode(w, w.reqs, got, ref["decode"], host["tokens"], host["mask"], label)
+    # every cell outside the active blocks (other columns, rows of no request) is untouched
+    gtok, _ = oracle.gather_active_blocks(w.reqs, w.L, got["tokens"])
+    gmsk, _ = oracle.gather_active_blocks(w.reqs, w.L, got["mask"])
+    np.testing.assert_array_equal(oracle.scatter_active_blocks(w.reqs, w.L, gtok, host["tokens"]), got["tokens"])
+    np.testing.assert_array_equal(oracle.scatter_active_blocks(w.reqs, w.L, gmsk, host["mask"]), got["mask"])
+    return stats
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
@@ -93,8 +80,9 @@ def test_fused_step_matches_oracle(ctx, cfg):
     got = snapshot(st)
     ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
                                   tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
-    nex = check_step(w, got, ref, host, f"cfg{cfg}")
-    say(f"  exempt requests: {nex}")
+    stats = check_step(w, got, ref, host, f"cfg{cfg}")
+    say(f"  decode: {stats}")
+    assert stats.band <= max(4, stats.positions // 50), stats
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -123,8 +111,8 @@ def test_fused_step_random_geometries(ctx, seed):
     got = snapshot(st)
     ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
                                   tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
-    nex = check_step(w, got, ref, host, f"random {seed}")
-    say(f"  exempt requests: {nex} of {n}")
+    stats = check_step(w, got, ref, host, f"random {seed}")
+    say(f"  decode: {stats}")
 
 
 @pytest.mark.parametrize("cfg,L", [(2, 16), (2, 64), (3, 16), (3, 64)])
@@ -141,81 +129,9 @@ def test_fused_step_block_length_sweep(ctx, cfg, L):
     got = snapshot(st)
     ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
                                   tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
-    nex = check_step(w, got, ref, host, w.name)
-    say(f"  exempt requests: {nex}")
-
-
-def test_churn_boundary_then_step_workload5(ctx):
-    """Workload 5 shapes (MHA 32 x 128, L = 32, g = 128, V = 126464, W = 384):
-    a seeded block-boundary churn plan rewrites the KV box in place (admitted
-    requests' staged KV copied into freed rows), then the fused step runs on
-    the new descriptors. The first 64 of the workload's 256 requests are used
-    (host-side input generation dominates the cost at 256); caches and the
-    dense state are checked in full, attention and decode on a seeded sample
-    of 24 requests."""
-    torch, bs, bstep = lazy()
-    w = synth.workload(5, layers=1)
-    w.reqs = w.reqs[:64].copy()
-    assert (w.reqs["row"] < 64).all()
-    w.R = 64
-    tok, msk, _ = synth.gen_state(w)
-    kc, vc = synth.gen_cache(w, 0)
-    plan = synth.churn_plan(w, w.reqs, tok, msk, step=1)      # rewrites tok/msk rows in place
-    say(f"[churn workload5] n={w.n} W={w.W} finish={plan.n_finish} complete={plan.n_complete}")
-    n_adm = len(plan.stage_reqs)
-    wst = int((plan.stage_reqs["p"] + plan.stage_reqs["g"]).max())
-    stg = [synth.gen_stage_row(w, 0, 1, a, wst) for a in range(n_adm)]
-    sk = np.stack([x[0] for x in stg])[None]                    # [1][n_adm][Hkv][Wst][D]
-    sv = np.stack([x[1] for x in stg])[None]
-    dkc, dvc = bstep.to_device(kc[None], "bf16"), bstep.to_device(vc[None], "bf16")
-    bstep.compact(ctx, plan.segs, 1, w.Hkv, w.D, "bf16", dkc, dvc, bstep.to_device(sk, "bf16"),
-                  bstep.to_device(sv, "bf16"), dkc, dvc)
-    reqs = plan.reqs
-    blk = oracle.gather_active_blocks(reqs, w.L, msk)[0].astype(bool)
-    q = synth.gen_q(w, 0)
-    kn, vn = synth.gen_kv_new(w, 0)
-    logits = synth.gen_logits(w, blk)
-    out = torch.full(q.shape, float("nan"), dtype=torch.bfloat16, device="cuda")
-    lay = bstep.Layer(bstep.to_device(q, "bf16"), bstep.to_device(kn, "bf16"), bstep.to_device(vn, "bf16"),
-                      dkc[0], dvc[0], out)
-    st = bstep.StepState(w.L, w.Hq, w.Hkv, w.D, w.V, w.dtype, w.R, w.W, bstep.to_device(tok), bstep.to_device(msk),
-                         [lay], bstep.to_device(logits, "bf16"), w.n, tau=w.tau, q_min=w.q_min,
-                         eos_id=w.eos_id).alloc()
-    bstep.run_step(ctx, st, reqs, want_conf=True)
-    torch.cuda.synchronize()
-    got = snapshot(st)
-
-    ck, cv = oracle.kv_scatter_compact(plan.segs, kc[None], vc[None], sk, sv, kc[None], vc[None])
-    sample = sorted(np.random.default_rng(55).choice(w.n, size=24, replace=False).tolist())
-    o_ref, kc2, vc2 = oracle.dual_cache_block_attention(reqs, w.L, q, kn, vn, ck[0], cv[0], dtype="bf16",
-                                                        write_back=True, only=sample)
-    np.testing.assert_array_equal(got["layers"][0]["k_cache"], kc2)   # compaction + write-through, every cell
-    np.testing.assert_array_equal(got["layers"][0]["v_cache"], vc2)
-    sub = reqs[sample]
-    check_attention(w, got["layers"][0]["out"][sample], o_ref[sample], reqs=sub, label="workload5 sample")
-    tok_c, _ = oracle.gather_active_blocks(reqs, w.L, tok)
-    msk_c, _ = oracle.gather_active_blocks(reqs, w.L, msk)
-    dec = oracle.parallel_decode(reqs, w.L, logits, tok_c, msk_c, tau=w.tau, q_min=w.q_min, eos_id=w.eos_id,
-                                 dtype="bf16", only=sample)
-    sub_dec = {k: v[sample] for k, v in dec.items() if isinstance(v, np.ndarray) and len(v) == w.n}
-    ex = exempt_requests(sub_dec, sub, w.L, w.tau, w.q_min)
-    gtok_c, _ = oracle.gather_active_blocks(reqs, w.L, got["tokens"])
-    gmsk_c, _ = oracle.gather_active_blocks(reqs, w.L, got["mask"])
-    for a, i in enumerate(sample):
-        m = dec["conf"][i] >= 0
-        assert np.array_equal(got["conf"][i] >= 0, m)
-        if m.any():
-            assert np.abs(got["conf"][i][m] - dec["conf"][i][m]).max() <= CONF_TOL
-        if a in ex:
-            continue
-        assert np.array_equal(gtok_c[i], dec["tokens"][i]), f"tokens differ (request {i})"
-        assert np.array_equal(gmsk_c[i], dec["masked"][i]), f"mask differs (request {i})"
-        for key in ("n_unmasked", "done", "eos_seen"):
-            assert got[key][i] == dec[key][i], f"{key} differs (request {i})"
-    # cells outside the active blocks are untouched by the step
-    np.testing.assert_array_equal(oracle.scatter_active_blocks(reqs, w.L, gtok_c, tok), got["tokens"])
-    np.testing.assert_array_equal(oracle.scatter_active_blocks(reqs, w.L, gmsk_c, msk), got["mask"])
-    say(f"  exempt sampled requests: {len(ex)}")
+    stats = check_step(w, got, ref, host, w.name)
+    say(f"  decode: {stats}")
+    assert stats.band <= max(4, stats.positions // 50), stats
 
 
 def test_fused_step_equals_separate_calls(ctx):

@@ -177,28 +177,80 @@ def masked_rows(blk):
     return int(blk.sum())
 
 
-def cpu_baseline(w, host, budget_s=12.0, max_reps=200):
-    """The oracle as it stands, timed on this host on the same inputs: whole
-    oracle steps are repeated until about budget_s seconds have passed."""
-    import oracle
+def blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
     except Exception:
-        threads = 1
+        return 1
+
+
+def host_description():
+    """The host the CPU baseline ran on: logical CPUs, the cores this process
+    may use, BLAS threads, NumPy version and CPU model."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"os_cpu_count": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas_threads": blas_threads(), "numpy": np.__version__, "cpu_model": model}
+
+
+def cpu_baseline(w, host, budget_s=12.0, max_reps=200):
+    """The oracle as it stands, timed on this host on the same inputs: whole
+    oracle steps are repeated until about budget_s seconds have passed.
+    Returns (record, the first step's result)."""
+    import oracle
+    threads = blas_threads()
     positions = sum(s[1] for s in w.spans())
     t0 = time.perf_counter()
     reps = 0
+    first = None
     while True:
-        oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
-                                tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+        r = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
+                                    tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+        first = r if first is None else first
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= max_reps:
             break
-    return {"value": round(positions * reps / el, 1), "unit": "positions/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{reps} whole oracle steps of the same workload ({positions} positions, "
-                      f"{w.layers} layer(s) each), fp64 NumPy, {el:.1f} s"}
+    rec = {"value": round(positions * reps / el, 1), "unit": "positions/s", "cores": threads, "kind": "oracle",
+           "sample": f"{reps} whole oracle steps of the same workload ({positions} positions, "
+                     f"{w.layers} layer(s) each), fp64 NumPy, {el:.1f} s"}
+    rec.update(host=host_description())
+    return rec, first
+
+
+def step_parity(w, host, got, ref):
+    """The GPU step (one step from the pristine state) against the oracle's
+    step on the same inputs: attention error per layer, cache cells that
+    differ, and the decode compared per position (a confidence within 1e-3 of
+    the threshold or of a tie at the selection boundary exempts that
+    position; every other decision must match bit for bit)."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from gpu_util import check_step_decode
+    import oracle
+    out = {"what": "one GPU step against the oracle's step on the same inputs"}
+    err = rel = 0.0
+    cells = 0
+    for g, r in zip(got["layers"], ref["layers"]):
+        o = oracle.widen(g["out"], w.dtype)
+        for i, (s0, B, _) in enumerate(w.spans()):
+            d = np.abs(o[i, :B] - r["out"][i, :B])
+            err = max(err, float(d.max()))
+            rel = max(rel, float(d.max() / max(np.abs(r["out"][i, :B]).max(), 1e-30)))
+        cells += int((g["k_cache"] != r["k_cache"]).sum() + (g["v_cache"] != r["v_cache"]).sum())
+    out.update(attention_max_abs_err=float(f"{err:.3g}"), attention_max_rel_err=float(f"{rel:.3g}"),
+               cache_cells_differing=cells)
+    try:
+        st = check_step_decode(w, w.reqs, got, ref["decode"], host["tokens"], host["mask"], "bench")
+        out.update(masked_positions=st.positions, exempt_positions=st.band, requests_with_open_count=st.open_requests,
+                   decision_mismatches=0)
+    except AssertionError as e:
+        out.update(decision_mismatches=1, first_mismatch=str(e)[:300])
+    return out
 
 
 KERNEL_SOURCES = {   # kernel name prefix -> sources whose change voids its counter-derived traffic
@@ -503,11 +555,7 @@ def lm_head_bench(args):
     if not args.no_cpu_baseline:
         import oracle
         print("[bench] timing the CPU oracle on a sample of the same inputs", file=sys.stderr, flush=True)
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = 1
+        threads = blas_threads()
         tic, reps, pos = time.perf_counter(), 0, 0
         while time.perf_counter() - tic < 12.0 and reps < w.n:
             oracle.lm_head_decode(w.reqs, w.L, hidden, wv, tok_c, msk_c, tau=w.tau, q_min=w.q_min,
@@ -515,7 +563,7 @@ def lm_head_bench(args):
             pos += w.spans()[reps][1]
             reps += 1
         el = time.perf_counter() - tic
-        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads),
+        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads), "host": host_description(),
                                "kind": "oracle",
                                "sample": f"{reps} requests' decoding steps with the output head (fp64), {el:.1f} s"}
     print(json.dumps(res), flush=True)
@@ -626,11 +674,7 @@ def refresh_bench(args):
     if not args.no_cpu_baseline:
         import oracle
         print("[bench] timing the CPU oracle on a sample of the same inputs", file=sys.stderr, flush=True)
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = 1
+        threads = blas_threads()
         order = np.argsort(lens)                  # shortest rows first: several requests fit the budget
         tic, reps, pos = time.perf_counter(), 0, 0
         while time.perf_counter() - tic < 12.0 and reps < w.n:
@@ -641,7 +685,7 @@ def refresh_bench(args):
             pos += lens[i]
             reps += 1
         el = time.perf_counter() - tic
-        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads),
+        res["cpu_baseline"] = {"value": round(pos / el, 1), "unit": "positions/s", "cores": int(threads), "host": host_description(),
                                "kind": "oracle",
                                "sample": f"the {reps} shortest requests' full-row refresh, all heads (fp64), "
                                          f"{el:.1f} s"}
@@ -770,11 +814,7 @@ def churn_bench(args):
     if not args.no_cpu_baseline:
         import oracle
         print("[bench] timing the CPU oracle on a sample of the same workload", file=sys.stderr, flush=True)
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = 1
+        threads = blas_threads()
         sample = list(range(8))
         q = synth.gen_q(w, 0)
         kn, vn = synth.gen_kv_new(w, 0)
@@ -804,7 +844,7 @@ def churn_bench(args):
         t_dec = time.perf_counter() - t0
         pos = sum(w.spans()[i][1] for i in sample)
         t_step = t_att * NL + t_dec
-        res["cpu_baseline"] = {"value": round(pos / t_step, 1), "unit": "positions/s", "cores": int(threads),
+        res["cpu_baseline"] = {"value": round(pos / t_step, 1), "unit": "positions/s", "cores": int(threads), "host": host_description(),
                                "kind": "oracle",
                                "sample": f"{len(sample)} requests: one layer's attention ({t_att:.2f} s) scaled to "
                                          f"{NL} layers, plus their decode ({t_dec:.2f} s); compaction not counted"}
@@ -856,82 +896,9 @@ def serve_bench(args):
         "ms_per_step": round(wall * 1e3 / res.steps, 4), "refresh_calls": res.refreshes}), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped, 4 = skewed Dream batch, "
-                         "5 = 32-layer LLaDA churn step with compaction)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
-    ap.add_argument("--pmc-calibration", action="store_true",
-                    help="run one 256 MiB device copy first (the reference kernel for FETCH_SIZE / WRITE_SIZE)")
-    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="turn two rocprofv3 --pmc runs into profiles/traffic_<workload>.md (no GPU needed)")
-    ap.add_argument("--serve", choices=["humaneval-256", "gsm8k-256", "mbpp-512", "truthfulqa-512"],
-                    help="closed-loop serving of a table-shaped request stream instead of the step bench")
-    ap.add_argument("--serve-requests", type=int, default=256)
-    ap.add_argument("--policy", choices=["budget", "fixed"], default="budget")
-    ap.add_argument("--batch", type=int, default=16, help="fixed cap, and B of Eq. 2")
-    ap.add_argument("--budget", type=int, default=0, help="Eq. 1 budget in tokens (default B * (avg prompt + limit))")
-    ap.add_argument("--rows", type=int, default=128, help="rows of the dense box under the budget policy")
-    ap.add_argument("--layers", type=int, default=1,
-                    help="attention layers per step (step mode: layers past the first are drawn on the device; "
-                         "--serve: model depth)")
-    ap.add_argument("--block-length", type=int, default=None,
-                    help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
-    ap.add_argument("--lm-head", action="store_true",
-                    help="time the output head fused with the decoding step against the unfused GEMM + decode")
-    ap.add_argument("--refresh", action="store_true",
-                    help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer; "
-                         "with --serve, rebuild the dual cache at every block start of the serving loop")
-    ap.add_argument("--no-library", action="store_true", help="--refresh: skip the library attention comparison")
-    ap.add_argument("--prefix-only", action="store_true",
-                    help="prefix-cache layout: keys end at the active block (no masked suffix)")
-    args = ap.parse_args()
-    if args.lm_head and not args.traffic_summary:
-        if args.gpus != 1:
-            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
-                  file=sys.stderr, flush=True)
-            sys.exit(2)
-        lm_head_bench(args)
-        return
-    if args.config == 5 and not args.traffic_summary and not args.serve:
-        if args.gpus != 1:
-            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
-                  file=sys.stderr, flush=True)
-            sys.exit(2)
-        churn_bench(args)
-        return
-    if args.refresh and not args.traffic_summary and not args.serve:
-        if args.gpus != 1:
-            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
-                  file=sys.stderr, flush=True)
-            sys.exit(2)
-        refresh_bench(args)
-        return
-    if args.serve:
-        if args.gpus != 1:
-            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
-                  file=sys.stderr, flush=True)
-            sys.exit(2)
-        serve_bench(args)
-        return
-    if args.traffic_summary:
-        import synth
-        name = synth.workload(args.config, block_length=args.block_length).name
-        if args.lm_head:
-            name += f"-lm-head-d{synth.LM_HEAD_DIM[args.config]}"
-        if args.refresh:
-            name += "-refresh"
-        traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
-        return
-    if args.gpus != 1:
-        print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
-              file=sys.stderr, flush=True)
-        sys.exit(2)
-
+def step_bench(args, cfg):
+    """Times the fused step on workload `cfg` (the regions described at the
+    top of this file) and returns its result record."""
     import torch
     import synth
     import paper_2607_08930_amd as bs
@@ -939,7 +906,7 @@ def main():
 
     assert torch.cuda.is_available()
     torch.cuda.set_device(0)
-    w = synth.workload(args.config, block_length=args.block_length)
+    w = synth.workload(cfg, block_length=args.block_length)
     if args.prefix_only:
         w.reqs = bstep.prefix_only(w.reqs, w.L)
         w.name += "-prefix-only"
@@ -1082,8 +1049,116 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline and args.layers == 1:
+        # one step from the pristine state, kept for the parity check
+        ctx = bs.Context(0)
+        st.tokens.copy_(tok0)
+        st.mask.copy_(msk0)
+        bstep.run_step(ctx, st, w.reqs, stream=stream, want_conf=True)
+        torch.cuda.synchronize()
+        got = dict(tokens=st.tokens.cpu().numpy(), mask=st.mask.cpu().numpy(), conf=st.conf.cpu().numpy(),
+                   n_unmasked=st.n_unmasked.cpu().numpy(), done=st.done.cpu().numpy(),
+                   eos_seen=st.eos_seen.cpu().numpy(),
+                   layers=[dict(out=bstep.to_host(x.out), k_cache=bstep.to_host(x.k_cache),
+                                v_cache=bstep.to_host(x.v_cache)) for x in st.layers])
+        ctx.close()
         print("[bench] timing the CPU oracle on the same inputs", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, host)
+        res["cpu_baseline"], ref = cpu_baseline(w, host)
+        res["parity"] = step_parity(w, host, got, ref)
+    del st, flush
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (2 = LLaDA-8B-shaped layer, 3 = Dream-7B-shaped, 4 = skewed Dream batch, "
+                         "5 = 32-layer LLaDA churn step with compaction)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", action="store_true",
+                    help="time only the chosen workload (the default run of workload 2 also times workload 3)")
+    ap.add_argument("--warm", action="store_true", help="skip the Infinity Cache flush between steps")
+    ap.add_argument("--pmc-calibration", action="store_true",
+                    help="run one 256 MiB device copy first (the reference kernel for FETCH_SIZE / WRITE_SIZE)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs into profiles/traffic_<workload>.md (no GPU needed)")
+    ap.add_argument("--serve", choices=["humaneval-256", "gsm8k-256", "mbpp-512", "truthfulqa-512"],
+                    help="closed-loop serving of a table-shaped request stream instead of the step bench")
+    ap.add_argument("--serve-requests", type=int, default=256)
+    ap.add_argument("--policy", choices=["budget", "fixed"], default="budget")
+    ap.add_argument("--batch", type=int, default=16, help="fixed cap, and B of Eq. 2")
+    ap.add_argument("--budget", type=int, default=0, help="Eq. 1 budget in tokens (default B * (avg prompt + limit))")
+    ap.add_argument("--rows", type=int, default=128, help="rows of the dense box under the budget policy")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="attention layers per step (step mode: layers past the first are drawn on the device; "
+                         "--serve: model depth)")
+    ap.add_argument("--block-length", type=int, default=None,
+                    help="re-block the workload's requests at L = 16 or 64 (block-length sweep)")
+    ap.add_argument("--lm-head", action="store_true",
+                    help="time the output head fused with the decoding step against the unfused GEMM + decode")
+    ap.add_argument("--refresh", action="store_true",
+                    help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer; "
+                         "with --serve, rebuild the dual cache at every block start of the serving loop")
+    ap.add_argument("--no-library", action="store_true", help="--refresh: skip the library attention comparison")
+    ap.add_argument("--prefix-only", action="store_true",
+                    help="prefix-cache layout: keys end at the active block (no masked suffix)")
+    args = ap.parse_args()
+    if args.lm_head and not args.traffic_summary:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        lm_head_bench(args)
+        return
+    if args.config == 5 and not args.traffic_summary and not args.serve:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        churn_bench(args)
+        return
+    if args.refresh and not args.traffic_summary and not args.serve:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        refresh_bench(args)
+        return
+    if args.serve:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        serve_bench(args)
+        return
+    if args.traffic_summary:
+        import synth
+        name = synth.workload(args.config, block_length=args.block_length).name
+        if args.lm_head:
+            name += f"-lm-head-d{synth.LM_HEAD_DIM[args.config]}"
+        if args.refresh:
+            name += "-refresh"
+        traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
+        return
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    res = step_bench(args, args.config)
+    # the Dream-7B-shaped layer is the other binding shape: the default run
+    # reports it in the same line, nested
+    if (args.config == 2 and not args.only and args.layers == 1 and args.block_length is None
+            and not args.prefix_only and not args.pmc_calibration):
+        second = step_bench(args, 3)
+        res["second_config"] = {k: second[k] for k in ("value", "unit", "ms_per_step", "config", "hbm", "roofline",
+                                                       "phases_ms", "kernel_GBps", "attention_tflops",
+                                                       "attention_mfma_frac", "step_ms_p10_p90", "back_to_back",
+                                                       "ms_per_step_warm", "copy_reference", "parity", "cpu_baseline")
+                                if k in second}
     print(json.dumps(res), flush=True)
 
 

@@ -88,8 +88,10 @@ typedef struct bs_ctx bs_ctx;
 
 /* Create a context bound to HIP device `device` (it becomes current while the
  * library works). The context owns only pinned host staging memory and device
- * upload slots for descriptors and work lists (allocated as calls need them).
- * *out is NULL on failure. */
+ * upload slots for descriptors and work lists (allocated as calls need them),
+ * plus four 512 KiB pinned stages for bs_mixed_state_step_noalloc, allocated
+ * here; it also resolves the device address of the library's static array
+ * for that call. *out is NULL on failure. */
 int bs_create(bs_ctx** out, int device);
 
 /* Wait for every upload slot to drain, then free the context (NULL is OK). */
@@ -347,6 +349,36 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
                         int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
                         uint8_t* done, uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* ws,
                         size_t ws_bytes, void* stream);
+
+/*
+ * bs_mixed_state_step for callers that cannot allocate device memory: code
+ * under HIP graph capture, serving loops that must not call hipMalloc, and
+ * harnesses that forbid allocation. Same arguments, rules and results as
+ * bs_mixed_state_step, without the workspace: the descriptors, the attention
+ * work list and the decode partials go to the library's static device array
+ * (8 MiB per GPU, held until the process ends), whose address the context
+ * resolved when it was created; the call itself allocates nothing and calls
+ * no allocating routine. Its host copy of the descriptors goes through one of
+ * four pinned stages that bs_create allocated; a call waits for the device
+ * only when all four are still being copied from.
+ * Limits (BS_ERR_UNSUPPORTED beyond them, before anything is enqueued):
+ * n * 20 bytes (rounded up to 16) plus n * Hkv * ceil(L / 32) * 32 bytes of
+ * work items (the ceil term only when (Hq / Hkv) * ceil(L / 32) > 8, else 1;
+ * no work items for BS_F32 or n_layers == 0) within 512 KiB; bs_decode_workspace_bytes(n, L,
+ * V, logits_dt) within 7.5 MiB.
+ * Every call on a GPU shares that GPU's array and leaves the last call's
+ * contents in it (nothing in it needs to start at zero): calls on one stream
+ * are ordered, but calls that may overlap on one GPU (other streams, other
+ * contexts or threads) race and must not be issued.
+ */
+int bs_mixed_state_step_noalloc(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers,
+                                int Hq, int Hkv, int D, bs_dtype dt, float scale, int write_back,
+                                const void* const* q, const void* const* k_new, const void* const* v_new,
+                                void* const* k_cache, void* const* v_cache, void* const* out, int V,
+                                bs_dtype logits_dt, const void* logits, int64_t logits_row_stride, int32_t* tokens,
+                                int64_t tokens_row_stride, uint8_t* masked, int64_t masked_row_stride, float tau,
+                                int32_t q_min, int32_t eos_id, int32_t* n_unmasked, uint8_t* done,
+                                uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* stream);
 
 /*
  * Phase timing of bs_mixed_state_step, bs_lm_head_decode and

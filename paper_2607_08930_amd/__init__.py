@@ -22,7 +22,7 @@ __all__ = [
     "bs_create", "bs_destroy", "bs_status_string", "bs_last_error", "bs_validate_requests",
     "bs_validate_segments",
     "bs_gather_active_blocks", "bs_scatter_active_blocks", "bs_gather_active_blocks_n",
-    "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_profile_begin", "bs_profile_end",
+    "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_mixed_state_step_noalloc", "bs_profile_begin", "bs_profile_end",
     "bs_sched_create", "bs_sched_destroy", "bs_sched_submit", "bs_sched_refill", "bs_sched_complete",
     "bs_sched_counts", "bs_sched_last_error", "Scheduler",
     "bs_attention_workspace_bytes",
@@ -84,6 +84,9 @@ _SIGS = {
     "bs_mixed_state_step": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32,
                                    _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i64, _vp, _i64, _vp, _i64,
                                    _f32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bs_mixed_state_step_noalloc": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32,
+                                           _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i64, _vp, _i64,
+                                           _vp, _i64, _f32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "bs_profile_begin": (_i32, [_vp, _i32]),
     "bs_profile_end": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_i32)]),
     "bs_sched_create": (_i32, [ctypes.POINTER(_vp), _vp]),
@@ -341,6 +344,21 @@ def bs_mixed_state_step(ctx, reqs, L, R, W, layers, Hq, Hkv, D, dt, scale, write
                                           _ptr(tokens), tokens_row_stride, _ptr(masked), masked_row_stride, tau,
                                           q_min, eos_id, _ptr(n_unmasked), _ptr(done), _ptr(eos_seen),
                                           _ptr(conf_out), _ptr(pos_out), _ptr(ws), ws_bytes, _stream(stream)), ctx)
+
+
+def bs_mixed_state_step_noalloc(ctx, reqs, L, R, W, layers, Hq, Hkv, D, dt, scale, write_back, V, logits_dt,
+                                logits, logits_row_stride, tokens, tokens_row_stride, masked, masked_row_stride, tau,
+                                q_min, eos_id, n_unmasked, done, eos_seen, conf_out, pos_out, stream=None):
+    """bs_mixed_state_step without a workspace; allocates nothing."""
+    r = _host(reqs, REQ_DTYPE)
+    nl = len(layers)
+    arrs = [(_vp * max(nl, 1))(*[_ptr(lay[t]) for lay in layers]) for t in range(6)]
+    return _check(lib.bs_mixed_state_step_noalloc(_ptr(ctx), _ptr(r), len(r), L, R, W, nl, Hq, Hkv, D, dt, scale,
+                                                  int(write_back), *arrs, V, logits_dt, _ptr(logits),
+                                                  logits_row_stride, _ptr(tokens), tokens_row_stride, _ptr(masked),
+                                                  masked_row_stride, tau, q_min, eos_id, _ptr(n_unmasked),
+                                                  _ptr(done), _ptr(eos_seen), _ptr(conf_out), _ptr(pos_out),
+                                                  _stream(stream)), ctx)
 
 
 PROFILE_PHASES = ("attention", "decode_rows", "decode_select")          # bs_mixed_state_step

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -66,8 +67,27 @@ struct Prof {
   bool on = false;
 };
 
+// ---- static device memory of the allocation-free step
+// The descriptors and attention work items of one call, then its decode
+// partials. Each GPU the library runs on holds its own copy of the array
+// until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for that device.
+constexpr size_t kStaticBlobBytes = size_t(512) << 10;
+constexpr size_t kStaticPartBytes = (size_t(8) << 20) - kStaticBlobBytes;
+constexpr int kStaticStages = 4;     // pinned host stages of a context (calls in flight before one waits)
+static __device__ __align__(256) unsigned char scratch[kStaticBlobBytes + kStaticPartBytes];
+
+struct StaticPath {
+  void* scratch = nullptr;                       // this device's `scratch` (device address)
+  void* stage[kStaticStages] = {};               // pinned host copies of a call's blob
+  hipEvent_t copied[kStaticStages] = {};         // recorded after the copy out of each stage
+  int next = 0;
+  std::unique_ptr<AttnItem[]> tmp;               // the work-list interleave's temporary
+};
+
 struct bs_ctx {
   int device = 0;
+  StaticPath stat;
   std::vector<std::unique_ptr<Slot>> slots;   // stable addresses: calls hold Slot*
   uint64_t tick = 0;
   std::string err;
@@ -302,45 +322,66 @@ int check_attention_tensors(bs_ctx* c, const void* q, const void* k_new, const v
   return BS_OK;
 }
 
-// Descriptors, then (bf16) the (request, KV head) work items, longest rows
-// first, so the tail of the grid is made of short items. When one wave owns
-// an item (G = 1, L <= 32), workgroup b takes the items ranked b, b + NB,
-// b + 2 NB, ... (NB workgroups): every CU streams about the same number of
-// bytes instead of some CUs getting only the longest rows.
-void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, bs_dtype dt) {
-  blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
-  if (dt == BS_BF16) {
-    std::vector<AttnItem> items;
-    items.reserve((size_t)n * Hkv);
-    // one workgroup per (request, KV head), or per (request, KV head, 32-row
-    // block) when the query group times the row blocks exceeds 8 waves
-    const int RB = (L + 31) / 32, split = (Hq / Hkv) * RB > 8 ? RB : 1;
-    for (int i = 0; i < n; ++i) {
-      const Geo gq = geo_of(reqs[i], L);
-      for (int h = 0; h < Hkv; ++h)
-        for (int rb = 0; rb < split; ++rb)
-          items.push_back(AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, rb});
-    }
-    std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) { return x.len > y.len; });
-    const size_t N = items.size();
-    if (Hq == Hkv && L <= 32 && N % kMhaWaves == 0) {
-      const size_t NB = N / kMhaWaves;
-      std::vector<AttnItem> mixed(N);
-      for (size_t b = 0; b < NB; ++b)
-        for (size_t j = 0; j < (size_t)kMhaWaves; ++j) mixed[b * kMhaWaves + j] = items[j * NB + b];
-      items.swap(mixed);
-    }
-    blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * items.size());
-    blob.meta[2] = (int)items.size();
+// The bf16 attention's (request, KV head) work items, longest rows first, so
+// the tail of the grid is made of short items: one workgroup per (request,
+// KV head), or per (request, KV head, 32-row block) when the query group
+// times the row blocks exceeds 8 waves. When one wave owns an item (G = 1,
+// L <= 32), workgroup b takes the items ranked b, b + NB, b + 2 NB, ... (NB
+// workgroups): every CU streams about the same number of bytes instead of
+// some CUs getting only the longest rows. Allocates nothing: `items` and
+// `tmp` hold attention_item_count(...) entries each.
+int attention_split(int L, int Hq, int Hkv) {
+  const int RB = (L + 31) / 32;
+  return (Hq / Hkv) * RB > 8 ? RB : 1;
+}
+
+size_t attention_item_count(int n, int L, int Hq, int Hkv, bs_dtype dt) {
+  return dt == BS_BF16 ? (size_t)n * Hkv * attention_split(L, Hq, Hkv) : 0;
+}
+
+void attention_items_into(AttnItem* items, AttnItem* tmp, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv) {
+  const int split = attention_split(L, Hq, Hkv);
+  size_t N = 0;
+  for (int i = 0; i < n; ++i) {
+    const Geo gq = geo_of(reqs[i], L);
+    for (int h = 0; h < Hkv; ++h)
+      for (int rb = 0; rb < split; ++rb) items[N++] = AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, rb};
+  }
+  // longest first; equal lengths keep the (request, head, row block) order
+  std::sort(items, items + N, [](const AttnItem& x, const AttnItem& y) {
+    if (x.len != y.len) return x.len > y.len;
+    if (x.req != y.req) return x.req < y.req;
+    if (x.kvh != y.kvh) return x.kvh < y.kvh;
+    return x.rb < y.rb;
+  });
+  if (Hq == Hkv && L <= 32 && N % kMhaWaves == 0) {
+    const size_t NB = N / kMhaWaves;
+    for (size_t b = 0; b < NB; ++b)
+      for (size_t j = 0; j < (size_t)kMhaWaves; ++j) tmp[b * kMhaWaves + j] = items[j * NB + b];
+    std::copy(tmp, tmp + N, items);
   }
 }
 
-AttnArgs attention_args(const Slot* sl, int L, int Hq, int Hkv, int D, int R, int W, float scale, int write_back) {
-  const char* base = static_cast<const char*>(sl->d);
+// Descriptors, then (bf16) the work items above.
+void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, bs_dtype dt) {
+  blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
+  if (dt == BS_BF16) {
+    const size_t N = attention_item_count(n, L, Hq, Hkv, dt);
+    std::vector<AttnItem> items(N), tmp(N);
+    attention_items_into(items.data(), tmp.data(), reqs, n, L, Hq, Hkv);
+    blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * N);
+    blob.meta[2] = (int)N;
+  }
+}
+
+// Launch arguments over a device blob at `dblob` laid out as `meta` says.
+AttnArgs attention_args(const void* dblob, const int* meta, int L, int Hq, int Hkv, int D, int R, int W, float scale,
+                        int write_back) {
+  const char* base = static_cast<const char*>(dblob);
   AttnArgs a{};
-  a.reqs = reinterpret_cast<const bs_req_desc*>(base + sl->meta[0]);
-  a.items = reinterpret_cast<const AttnItem*>(base + sl->meta[1]);
-  a.n_items = sl->meta[2];
+  a.reqs = reinterpret_cast<const bs_req_desc*>(base + meta[0]);
+  a.items = reinterpret_cast<const AttnItem*>(base + meta[1]);
+  a.n_items = meta[2];
   a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = Hq / Hkv; a.RB = (L + 31) / 32; a.R = R; a.W = W;
   a.RBW = a.G * a.RB > 8 ? 1 : a.RB;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
@@ -395,8 +436,9 @@ size_t decode_ws_bytes(int n, int L, int V, bs_dtype dt) {
   return dec_workspace_bytes(n, L, dec_parts(V, dtype_bytes(dt)));
 }
 
+// skip_ws: the caller checks (or provides) the workspace itself
 int check_decode(bs_ctx* c, int n, int L, int V, bs_dtype logits_dt, int64_t logits_row_stride, float tau,
-                 int q_min, const void* ws, size_t ws_bytes) {
+                 int q_min, const void* ws, size_t ws_bytes, bool skip_ws = false) {
   const int eb = dtype_bytes(logits_dt);
   if (!eb) return fail(c, BS_ERR_INVALID_ARG, "bad dtype %d", (int)logits_dt);
   if (L > 64) return fail(c, BS_ERR_UNSUPPORTED, "decode needs L <= 64 (L=%d)", L);
@@ -408,6 +450,7 @@ int check_decode(bs_ctx* c, int n, int L, int V, bs_dtype logits_dt, int64_t log
   if (logits_row_stride < V || (logits_row_stride * eb) % 16)
     return fail(c, BS_ERR_INVALID_ARG, "logits row stride %lld must be >= V and a multiple of 16 bytes",
                 (long long)logits_row_stride);
+  if (skip_ws) return BS_OK;
   const size_t need = decode_ws_bytes(n, L, V, logits_dt);
   if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   return BS_OK;
@@ -511,6 +554,37 @@ hipError_t prof_mark(bs_ctx* c, int phase, hipStream_t s) {
   return hipEventRecord(p.ev[(size_t)p.used * (kProfPhases + 1) + phase], s);
 }
 
+// Set-up of the allocation-free step for context c, on its device: the
+// device address of `scratch` (resolved once per device and kept), the
+// context's pinned stages and their events, and the interleave temporary.
+std::mutex g_scratch_mu;
+void* g_scratch_addr[64] = {};
+
+int static_setup(bs_ctx* c) {
+  if (c->device >= 64) return fail(nullptr, BS_ERR_UNSUPPORTED, "device %d: the library serves devices 0..63", c->device);
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(nullptr, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[c->device]) {
+      void* p = nullptr;
+      hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p) return hip_fail(nullptr, e != hipSuccess ? e : hipErrorInvalidSymbol,
+                                                 "hipGetSymbolAddress(scratch)");
+      g_scratch_addr[c->device] = p;
+    }
+    c->stat.scratch = g_scratch_addr[c->device];
+  }
+  for (int k = 0; k < kStaticStages; ++k) {
+    hipError_t e = hipHostMalloc(&c->stat.stage[k], kStaticBlobBytes, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "hipHostMalloc(no-alloc stage)");
+    e = hipEventCreateWithFlags(&c->stat.copied[k], hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "hipEventCreate(no-alloc stage)");
+  }
+  c->stat.tmp.reset(new AttnItem[kStaticBlobBytes / sizeof(AttnItem)]);
+  return BS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -524,6 +598,11 @@ int bs_create(bs_ctx** out, int device) {
   if (device < 0 || device >= count) return fail(nullptr, BS_ERR_INVALID_ARG, "device %d of %d", device, count);
   bs_ctx* c = new bs_ctx();
   c->device = device;
+  int st = static_setup(c);
+  if (st) {
+    bs_destroy(c);
+    return st;
+  }
   *out = c;
   return BS_OK;
 }
@@ -532,6 +611,13 @@ int bs_destroy(bs_ctx* c) {
   if (!c) return BS_OK;
   DeviceGuard dg(c->device);
   for (hipEvent_t e : c->prof.ev) (void)hipEventDestroy(e);
+  for (int k = 0; k < kStaticStages; ++k) {
+    if (c->stat.copied[k]) {
+      (void)hipEventSynchronize(c->stat.copied[k]);
+      (void)hipEventDestroy(c->stat.copied[k]);
+    }
+    if (c->stat.stage[k]) (void)hipHostFree(c->stat.stage[k]);
+  }
   for (auto& p : c->slots) {
     Slot& sl = *p;
     if (sl.live) (void)hipEventSynchronize(sl.done);
@@ -668,7 +754,7 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
               [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
   if (st) return st;
-  AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);
+  AttnArgs a = attention_args(sl->d, sl->meta, L, Hq, Hkv, D, R, W, scale, write_back);
   a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
   (void)ws;
   hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
@@ -865,14 +951,13 @@ int bs_dual_cache_refresh(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int 
 }
 
 // ------------------------------------------------------------------ fused step
-int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
-                        int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
-                        const void* const* k_new, const void* const* v_new, void* const* k_cache,
-                        void* const* v_cache, void* const* out, int V, bs_dtype logits_dt, const void* logits,
-                        int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
-                        int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
-                        uint8_t* done, uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* ws,
-                        size_t ws_bytes, void* stream) {
+// Checks shared by bs_mixed_state_step and its allocation-free variant (the
+// decode workspace is checked by the caller).
+static int check_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq, int Hkv,
+                      int D, bs_dtype dt, const void* const* q, const void* const* k_new, const void* const* v_new,
+                      void* const* k_cache, void* const* v_cache, void* const* out, int V, bs_dtype logits_dt,
+                      int64_t logits_row_stride, int64_t tokens_row_stride, int64_t masked_row_stride, float tau,
+                      int32_t q_min) {
   if (!c) return fail(nullptr, BS_ERR_INVALID_ARG, "ctx is NULL");
   int st = check_reqs(c, reqs, n, L, R, W);
   if (st) return st;
@@ -881,7 +966,8 @@ int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R,
     st = check_attention(c, n, L, Hq, Hkv, D, dt);
     if (st) return st;
   }
-  st = check_decode(c, n, L, V, logits_dt, logits_row_stride, tau, q_min, ws, ws_bytes);
+  // the workspace is checked separately: pass a size that always suffices
+  st = check_decode(c, n, L, V, logits_dt, logits_row_stride, tau, q_min, nullptr, 0, true);
   if (st) return st;
   if (tokens_row_stride < W || masked_row_stride < W)
     return fail(c, BS_ERR_INVALID_ARG, "token/mask row strides must be >= W");
@@ -892,17 +978,21 @@ int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R,
     st = check_attention_tensors(c, q[l], k_new[l], v_new[l], k_cache[l], v_cache[l], out[l], l);
     if (st) return st;
   }
-  st = check_decode_tensors(c, logits, tokens, masked, n_unmasked, done, eos_seen, conf_out, pos_out, ws);
-  if (st) return st;
-  DeviceGuard dg(c->device);
-  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
-              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
-  if (st) return st;
+  return BS_OK;
+}
+
+// Enqueues the step over the device blob `dblob` (descriptors and attention
+// work items, laid out as `meta` says) with decode partials in `ws`.
+static hipError_t step_launch(bs_ctx* c, const void* dblob, const int* meta, int n, int L, int R, int W, int n_layers,
+                              int Hq, int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
+                              const void* const* k_new, const void* const* v_new, void* const* k_cache,
+                              void* const* v_cache, void* const* out, int V, bs_dtype logits_dt, const void* logits,
+                              int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
+                              int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id,
+                              int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen, float* conf_out,
+                              int32_t* pos_out, void* ws, hipStream_t s) {
   hipError_t e = prof_mark(c, 0, s);
-  AttnArgs a = attention_args(sl, L, Hq, Hkv, D, R, W, scale, write_back);
+  AttnArgs a = attention_args(dblob, meta, L, Hq, Hkv, D, R, W, scale, write_back);
   for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
     a.q = q[l]; a.k_new = k_new[l]; a.v_new = v_new[l]; a.k_cache = k_cache[l]; a.v_cache = v_cache[l]; a.out = out[l];
     e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
@@ -917,7 +1007,104 @@ int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R,
     e = launch_decode_marked(d, logits_dt, s, [&](int ph) { return prof_mark(c, ph, s); });
   }
   if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;
+  return e;
+}
+
+int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
+                        int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
+                        const void* const* k_new, const void* const* v_new, void* const* k_cache,
+                        void* const* v_cache, void* const* out, int V, bs_dtype logits_dt, const void* logits,
+                        int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
+                        int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id, int32_t* n_unmasked,
+                        uint8_t* done, uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int st = check_step(c, reqs, n, L, R, W, n_layers, Hq, Hkv, D, dt, q, k_new, v_new, k_cache, v_cache, out, V,
+                      logits_dt, logits_row_stride, tokens_row_stride, masked_row_stride, tau, q_min);
+  if (st) return st;
+  st = check_decode(c, n, L, V, logits_dt, logits_row_stride, tau, q_min, ws, ws_bytes, false);
+  if (st) return st;
+  if (n == 0) return BS_OK;
+  st = check_decode_tensors(c, logits, tokens, masked, n_unmasked, done, eos_seen, conf_out, pos_out, ws);
+  if (st) return st;
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Slot* sl = nullptr;
+  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
+              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
+  if (st) return st;
+  hipError_t e = step_launch(c, sl->d, sl->meta, n, L, R, W, n_layers, Hq, Hkv, D, dt, scale, write_back, q, k_new,
+                             v_new, k_cache, v_cache, out, V, logits_dt, logits, logits_row_stride, tokens,
+                             tokens_row_stride, masked, masked_row_stride, tau, q_min, eos_id, n_unmasked, done,
+                             eos_seen, conf_out, pos_out, ws, s);
   return finish(c, sl, s, e, "step launch");
+}
+
+// ------------------------------------------------------------------ fused step without allocation
+// The step for callers that cannot allocate: the descriptors, the attention
+// work items and the decode partials live in this device's `scratch` array
+// (the library's static device memory), whose address set-up resolved. The
+// blob is built in one of the context's pinned stages (allocated by
+// bs_create) and copied into the array on the call's stream.
+int bs_mixed_state_step_noalloc(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers,
+                                int Hq, int Hkv, int D, bs_dtype dt, float scale, int write_back,
+                                const void* const* q, const void* const* k_new, const void* const* v_new,
+                                void* const* k_cache, void* const* v_cache, void* const* out, int V,
+                                bs_dtype logits_dt, const void* logits, int64_t logits_row_stride, int32_t* tokens,
+                                int64_t tokens_row_stride, uint8_t* masked, int64_t masked_row_stride, float tau,
+                                int32_t q_min, int32_t eos_id, int32_t* n_unmasked, uint8_t* done,
+                                uint8_t* eos_seen, float* conf_out, int32_t* pos_out, void* stream) {
+  int st = check_step(c, reqs, n, L, R, W, n_layers, Hq, Hkv, D, dt, q, k_new, v_new, k_cache, v_cache, out, V,
+                      logits_dt, logits_row_stride, tokens_row_stride, masked_row_stride, tau, q_min);
+  if (st) return st;
+  StaticPath& sp = c->stat;
+  const size_t n_items = n_layers > 0 ? attention_item_count(n, L, Hq, Hkv, dt) : 0;   // no attention, no work list
+  const size_t items_off = ((size_t)n * sizeof(bs_req_desc) + 15) & ~size_t(15);
+  const size_t blob_bytes = items_off + n_items * sizeof(AttnItem);
+  if (blob_bytes > kStaticBlobBytes)
+    return fail(c, BS_ERR_UNSUPPORTED, "descriptors and work items (%zu bytes for n=%d, Hkv=%d) exceed the %zu "
+                "bytes the no-alloc step reserves for them", blob_bytes, n, Hkv, kStaticBlobBytes);
+  const size_t part_bytes = decode_ws_bytes(n, L, V, logits_dt);
+  if (part_bytes > kStaticPartBytes)
+    return fail(c, BS_ERR_UNSUPPORTED, "decode partials (%zu bytes for n=%d, L=%d, V=%d) exceed the %zu bytes "
+                "the no-alloc step reserves for them", part_bytes, n, L, V, kStaticPartBytes);
+  if (n == 0) return BS_OK;
+  unsigned char* dscratch = static_cast<unsigned char*>(sp.scratch);
+  st = check_decode_tensors(c, logits, tokens, masked, n_unmasked, done, eos_seen, conf_out, pos_out,
+                            dscratch + kStaticBlobBytes);
+  if (st) return st;
+  DeviceGuard dg(c->device);
+  if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // a stage whose previous copy has completed; only when every stage is
+  // still being copied from does the call wait, for the oldest
+  int k = -1;
+  for (int t = 0; t < kStaticStages && k < 0; ++t) {
+    const int cand = (sp.next + t) % kStaticStages;
+    const hipError_t q_ = hipEventQuery(sp.copied[cand]);
+    if (q_ == hipSuccess) k = cand;
+    else if (q_ != hipErrorNotReady) return hip_fail(c, q_, "hipEventQuery(stage)");
+  }
+  if (k < 0) {
+    k = sp.next;
+    hipError_t e = hipEventSynchronize(sp.copied[k]);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize(stage)");
+  }
+  sp.next = (k + 1) % kStaticStages;
+  unsigned char* h = static_cast<unsigned char*>(sp.stage[k]);
+  std::memcpy(h, reqs, sizeof(bs_req_desc) * n);
+  if (n_items) attention_items_into(reinterpret_cast<AttnItem*>(h + items_off), sp.tmp.get(), reqs, n, L, Hq, Hkv);
+  const int meta[4] = {0, (int)items_off, (int)n_items, 0};
+  hipError_t e = hipMemcpyAsync(dscratch, h, blob_bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync(scratch)");
+  e = hipEventRecord(sp.copied[k], s);
+  if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord(stage)");
+  e = step_launch(c, dscratch, meta, n, L, R, W, n_layers, Hq, Hkv, D, dt, scale, write_back, q, k_new, v_new,
+                  k_cache, v_cache, out, V, logits_dt, logits, logits_row_stride, tokens, tokens_row_stride, masked,
+                  masked_row_stride, tau, q_min, eos_id, n_unmasked, done, eos_seen, conf_out, pos_out,
+                  dscratch + kStaticBlobBytes, s);
+  if (e != hipSuccess) return hip_fail(c, e, "no-alloc step launch");
+  return BS_OK;
 }
 
 int bs_profile_begin(bs_ctx* c, int max_steps) {

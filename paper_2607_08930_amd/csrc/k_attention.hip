@@ -6,8 +6,9 @@
 // masked suffix [s + B, p + g). Key t of the row is therefore fetched either
 // from cache cell off + t of the request's dense row or from fresh row t - s;
 // the stale block slot and the padding are never read. With write_back the
-// fresh rows are also stored into the cache slot as they stream past
-// (in-place KV update at the physical offsets of the active block).
+// fresh rows are also stored into the cache slot from the LDS tile that holds
+// them (in-place KV update at the physical offsets of the active block), so
+// they are read from memory once.
 //
 // bf16 path (gfx950 MFMA): one workgroup per (request, KV head) and one wave
 // per (query head of the group, 32-row block of the active block), so the K/V
@@ -251,6 +252,37 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       wait_vm_c<3 * PB>();
   };
 
+  // In-place KV update. Group loop: the fresh block rows that a tile holds
+  // (keys [tb, tb + KT) within [bs, be), staged from k_new / v_new) go into
+  // the cache slot [off + s, off + s + B) straight from LDS, so they are read
+  // from memory once. A store counts in vmcnt like the DMA, so a store issued
+  // in the loop would make the next stage wait drain it too: the stores come
+  // from the waves that issue no DMA (when the group has any). The
+  // single-wave loop stores the rows after its last wait instead (measured
+  // faster there than holding them in registers through the loop). Only the
+  // row-block-0 workgroup of an item stores them.
+  const bool do_wb = a.write_back && it.rb == 0;
+  uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
+  uint16_t* vcw = static_cast<uint16_t*>(a.v_cache) + cache_off;
+  // chunk cid of the tile's fresh rows (K then V) by lane
+  // (wg - w0) * 64 + lane of the storing waves [w0, GW)
+  auto write_back_tile = [&](const uint16_t* st, int tb) {
+    const int r0 = max(bs, tb) - tb, r1 = min(be, tb + KT) - tb;
+    const int w0 = GW > NI ? NI : 0;
+    if (!do_wb || r0 >= r1 || wg < w0) return;
+    const int nc = (r1 - r0) * NCH;               // chunks per tensor
+    const int gt = (wg - w0) * 64 + lane, gth = (GW - w0) * 64;
+#pragma unroll
+    for (int tensor = 0; tensor < 2; ++tensor) {
+      const uint16_t* src = st + tensor * TILE;
+      uint16_t* dst = tensor ? vcw : kcw;
+      for (int cid = gt; cid < nc; cid += gth) {
+        const int row = r0 + cid / NCH, c = cid % NCH;
+        const v4u v = *reinterpret_cast<const v4u*>(src + row * D + ((c ^ swz<NCH>(row)) * 8));
+        st16(dst + (int64_t)(tb + row) * D + c * 8, v);
+      }
+    }
+  };
   const int ntiles = (len + KT - 1) / KT;
   // prologue: stages 0 .. NS-2 (issued before anything else so the first
   // tiles are in flight while the queries load)
@@ -386,6 +418,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       const uint16_t* vt = ring + (tile % NS) * STAGE + TILE;
       pv(vt, pa0, pa1);
       pv(vt + 32 * D, pb0, pb1);
+      write_back_tile(ring + (tile % NS) * STAGE, tb);
     }
   } else {
     for (int tile = 0; tile < ntiles; ++tile) {
@@ -458,31 +491,29 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
     }
   }
   const float lt = lsum + __shfl_xor(lsum, 32, 64);
-  // in-place KV update: the group's waves store the fresh block rows of this
-  // KV head into the cache slot [off + s, off + s + B) (one workgroup per
-  // KV head does it when the row blocks are split over several)
-  if (a.write_back && it.rb == 0) {
-    constexpr int MAXWB = 32 * D / 8 / 64;          // per wave, for a 32-row block
-    uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
-    uint16_t* vcw = static_cast<uint16_t*>(a.v_cache) + cache_off;
-    const int nch = it.B * (D / 8);
-    const int gt = wg * 64 + lane, gth = GW * 64;
-    for (int base = 0; base < nch; base += gth * MAXWB) {
-      v4u kw[MAXWB], vw[MAXWB];
+  // single-wave loop: the in-place KV update after the last wait (the rows
+  // are read again, from k_new / v_new, and stored into the cache slot)
+  if constexpr (!SHARED) {
+    if (do_wb) {
+      constexpr int MAXWB = 32 * D / 8 / 64;          // 16-byte chunks per lane for a 32-row block
+      const int nch = it.B * (D / 8);
+      for (int base = 0; base < nch; base += 64 * MAXWB) {
+        v4u kw[MAXWB], vw[MAXWB];
 #pragma unroll
-      for (int u = 0; u < MAXWB; ++u) {
-        const int cid = min(base + gt + u * gth, nch - 1);
-        const int64_t src = (int64_t)(cid / (D / 8)) * fstride + (cid % (D / 8)) * 8;
-        kw[u] = ld16(knb + src);
-        vw[u] = ld16(vnb + src);
-      }
+        for (int u = 0; u < MAXWB; ++u) {
+          const int cid = min(base + lane + u * 64, nch - 1);
+          const int64_t src = (int64_t)(cid / (D / 8)) * fstride + (cid % (D / 8)) * 8;
+          kw[u] = ld16(knb + src);
+          vw[u] = ld16(vnb + src);
+        }
 #pragma unroll
-      for (int u = 0; u < MAXWB; ++u) {
-        const int cid = base + gt + u * gth;
-        if (cid < nch) {
-          const int64_t dst = (int64_t)(bs + cid / (D / 8)) * D + (cid % (D / 8)) * 8;
-          st16(kcw + dst, kw[u]);
-          st16(vcw + dst, vw[u]);
+        for (int u = 0; u < MAXWB; ++u) {
+          const int cid = base + lane + u * 64;
+          if (cid < nch) {
+            const int64_t dst = (int64_t)(bs + cid / (D / 8)) * D + (cid % (D / 8)) * 8;
+            st16(kcw + dst, kw[u]);
+            st16(vcw + dst, vw[u]);
+          }
         }
       }
     }

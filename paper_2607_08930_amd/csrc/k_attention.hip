@@ -518,10 +518,18 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       }
     }
   }
-  // lane (g, n): O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4][query n]
-  if (j < a.L) {
+  // Output: lane (g, n) holds O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4]
+  // [query n]. The wave's 32 x D tile is staged row-major in LDS (rows padded
+  // by 16 bytes against bank conflicts) and stored as whole rows, 16 bytes per
+  // lane, instead of 8-byte pieces scattered over 32 rows. The stores are
+  // non-temporal: the output is not read again by the step, and whole lines
+  // written around the L2 leave no dirty lines for the kernels that follow
+  // to evict (measured: the Dream-7B step's decode rows 61.5 -> 57.7 us).
+  if constexpr (SHARED) __syncthreads();          // every wave is done with the ring
+  constexpr int SROW = D + 8;                     // staged row stride (elements)
+  uint16_t* stg = ring + (SHARED ? wg * 32 * SROW : 0);
+  {
     const float inv = (j < it.B) ? 1.0f / lt : 0.0f;
-    uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)it.req * a.L + j) * a.Hq + h) * D;
     typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -533,8 +541,21 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
         const __bf16 b3 = (__bf16)(o[dt][4 * rq + 3] * inv);
         const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
         const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) | ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
-        *reinterpret_cast<v2u*>(op + dt * 32 + 8 * rq + 4 * g) = v2u{w0, w1};
+        *reinterpret_cast<v2u*>(stg + n * SROW + dt * 32 + 8 * rq + 4 * g) = v2u{w0, w1};
       }
+  }
+  {
+    constexpr int RPW = 64 / NCH;                 // rows per wave instruction
+    const int jb = (it.rb + wg % a.RBW) * 32;     // first block row of this wave
+#pragma unroll
+    for (int k = 0; k < 32 / RPW; ++k) {
+      const int row = k * RPW + lane / NCH, c = lane % NCH;
+      const v4u v = *reinterpret_cast<const v4u*>(stg + row * SROW + c * 8);
+      if (jb + row < a.L) {
+        uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)it.req * a.L + jb + row) * a.Hq + h) * D;
+        __builtin_nontemporal_store(v, reinterpret_cast<v4u*>(op + c * 8));
+      }
+    }
   }
 }
 

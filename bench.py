@@ -389,6 +389,163 @@ def traffic_summary(args, workload):
     print("\n".join(lines))
 
 
+COUNTER_PASSES = (
+    ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAVE_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA",
+     "SQ_ACTIVE_INST_VALU", "SQ_INSTS_LDS", "GRBM_GUI_ACTIVE"),
+    ("SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_ACTIVE_INST_LDS",
+     "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_INSTS_VALU_TRANS_F32", "SQ_ACTIVE_INST_ANY", "GRBM_GUI_ACTIVE"),
+)
+CU_NUM, SIMD_NUM = 256, 1024
+
+
+def counter_summary(args, workload):
+    """Counter CSVs of the two COUNTER_PASSES runs -> profiles/counters_<workload>.md:
+    per library kernel, the mean per dispatch of each counter and the derived
+    shares (the vendor's MfmaUtil, VALUBusy, LdsUtil and LdsBankConflict
+    expressions; wait and co-execution shares of wave and MFMA cycles)."""
+    import csv
+    import glob
+    vals, dur = {}, {}
+    n_xcc = 8
+    for fn in glob.glob(os.path.join(args.counter_summary[0], "**", "*agent_info.csv"), recursive=True):
+        for r in csv.DictReader(open(fn)):
+            if r.get("Agent_Type") == "GPU":
+                n_xcc = int(r["Num_Xcc"])
+    for d in args.counter_summary:
+        for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(fn)):
+                name = r["Kernel_Name"].replace("void ", "").replace("bs::(anonymous namespace)::", "").split("(")[0]
+                if not any(name.startswith(k) for k in KERNEL_SOURCES):
+                    continue
+                vals.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                key = (d, r["Dispatch_Id"])
+                dur.setdefault(name, {})[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    mode = " --lm-head" if args.lm_head else (" --refresh" if args.refresh else "")
+    lines = [f"# Hardware counters per launch: {workload}", "",
+             "Commands (repo root as `$R`, one MI355X; counters sampled per dispatch, values summed over the",
+             "chip by rocprofv3, then averaged over the dispatches of each kernel):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp"]
+    for k, pas in enumerate(COUNTER_PASSES):
+        lines.append(f"rocprofv3 --pmc {' '.join(pas)} -d <dir{k}> -o run --output-format csv -- "
+                     f"python3 $R/bench.py{mode} --config {args.config} --only --steps 5 --warmup 1 "
+                     f"--no-cpu-baseline --pmc-calibration")
+    lines += [f"python3 $R/bench.py{mode} --config {args.config} --counter-summary <dir0> <dir1>", "```", "",
+              "Derived (GRBM_GUI_ACTIVE = active cycles of the dispatch, per XCC: rocprofv3 sums the 8 XCCs;",
+              "it also counts a fixed sampling window of about 10 us, so short kernels read a low clock;",
+              "256 CUs, 1024 SIMDs):",
+              "* MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 1024) (vendor MfmaUtil);",
+              "* VALU busy = SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE x 256) (vendor VALUBusy);",
+              "* LDS busy = SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE x 256) (vendor LdsUtil); bank conflicts =",
+              "  SQ_LDS_BANK_CONFLICT / (SQ_LDS_IDX_ACTIVE - SQ_LDS_BANK_CONFLICT) (vendor LdsBankConflict);",
+              "* waits = SQ_WAIT_ANY / SQ_WAVE_CYCLES and SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES (shares of wave",
+              "  time; the two passes are separate runs of the same launches);",
+              "* co-issue = SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES (MFMA-busy cycles in which a",
+              "  VALU instruction also issued); clock = GRBM_GUI_ACTIVE / duration.", "",
+              "| kernel | launches | us | clock GHz | MFMA busy | VALU busy | LDS busy | bank confl. | waits any | "
+              "waits issue | co-issue | MFMA insts | VALU insts | trans. insts | LDS insts |",
+              "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    keep = []
+    for name in sorted(vals):
+        v = {c: float(np.mean(x)) for c, x in vals[name].items()}
+        us = float(np.mean(list(dur[name].values())))
+        g = v.get("GRBM_GUI_ACTIVE", float("nan")) / n_xcc      # rocprofv3 sums the XCCs' (equal) counts
+
+        def pct(x):
+            return f"{100 * x:.1f}%" if x == x else "-"
+
+        get = lambda c: v.get(c, float("nan"))
+        mfma = get("SQ_VALU_MFMA_BUSY_CYCLES") / (g * SIMD_NUM)
+        valu = get("SQ_ACTIVE_INST_VALU") / (g * CU_NUM)
+        lds = get("SQ_LDS_IDX_ACTIVE") / (g * CU_NUM)
+        bc = get("SQ_LDS_BANK_CONFLICT") / max(get("SQ_LDS_IDX_ACTIVE") - get("SQ_LDS_BANK_CONFLICT"), 1.0)
+        wa = get("SQ_WAIT_ANY") / get("SQ_WAVE_CYCLES")
+        wi = get("SQ_WAIT_INST_ANY") / get("SQ_WAVE_CYCLES")
+        co = get("SQ_VALU_MFMA_COEXEC_CYCLES") / max(get("SQ_VALU_MFMA_BUSY_CYCLES"), 1.0)
+        n_disp = len(dur[name])
+        lines.append(f"| `{name}` | {n_disp} | {us:.2f} | {g / us / 1e3:.2f} | {pct(mfma)} | {pct(valu)} | "
+                     f"{pct(lds)} | {pct(bc)} | {pct(wa)} | {pct(wi)} | {pct(co)} | {get('SQ_INSTS_MFMA'):.0f} | "
+                     f"{get('SQ_INSTS_VALU'):.0f} | {get('SQ_INSTS_VALU_TRANS_F32'):.0f} | {get('SQ_INSTS_LDS'):.0f} |")
+        pref = next(k for k in KERNEL_SOURCES if name.startswith(k))
+        keep.append(f"`counters {pref} {source_hash(pref)}`")
+    lines += ["", "Sources of each kernel when measured (hash; a changed kernel makes the row stale):", ""] + \
+             [k + "  " for k in sorted(set(keep))] + [""]
+    open(os.path.join(ROOT, "profiles", f"counters_{workload}.md"), "w").write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def kernel_summary(args):
+    """A rocprofv3 --kernel-trace CSV of a bench run -> profiles/<name>_kernel_stats.md:
+    per kernel, launches and mean / min / max duration; per step (one attention
+    launch followed by the decode row reductions and the selection), the median
+    of each kernel and of the gaps between them, by attention kernel."""
+    import csv
+    import glob
+    d, name = args.kernel_summary
+    cmd = args.bench_args
+    rows = []
+    for fn in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        rows += list(csv.DictReader(open(fn)))
+    ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]) for r in rows)
+
+    def short(n):
+        n = n.replace("void ", "").replace("bs::(anonymous namespace)::", "")
+        if "reduce_kernel" in n:
+            return "torch reduce_kernel (cache sweep / state restore, outside timing)"
+        if "elementwise" in n or "FillFunctor" in n or n.startswith("__amd_rocclr"):
+            return "torch / runtime copy or fill (outside timing)"
+        return n.split("(")[0]
+
+    # step triples (attention, decode rows, selection), by attention kernel
+    steps = {}
+    tag = {}
+    for a, b, c in zip(ks, ks[1:], ks[2:]):
+        if "k_attn" in a[2] and "k_decode_parts" in b[2] and "k_decode_select" in c[2]:
+            ka = short(a[2])
+            steps.setdefault(ka, []).append(((a[1] - a[0]) / 1e3, (b[0] - a[1]) / 1e3, (b[1] - b[0]) / 1e3,
+                                             (c[0] - b[1]) / 1e3, (c[1] - c[0]) / 1e3, (c[1] - a[0]) / 1e3))
+            tag[b] = tag[c] = f" (step of {ka})"
+    per = {}
+    for k in ks:
+        per.setdefault(short(k[2]) + tag.get(k, ""), []).append((k[1] - k[0]) / 1e3)
+    lines = [f"# Kernel durations: {name}", "", "Commands (repo root as `$R`, one MI355X):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp",
+             f"rocprofv3 --kernel-trace --stats -d <dir> -o run --output-format csv -- python3 $R/bench.py {cmd}",
+             f"python3 $R/bench.py --kernel-summary <dir> {name} --bench-args='{cmd}'", "```", "",
+             "| kernel | launches | mean us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for k in sorted(per, key=lambda k: -sum(per[k])):
+        v = per[k]
+        lines.append(f"| `{k}` | {len(v)} | {np.mean(v):.2f} | {np.min(v):.2f} | {np.max(v):.2f} |")
+    lines += ["", "Per step (attention launch, then the decode row reductions and the selection): median over the",
+              "steps of every timed region of the run (isolated, phase ring, warm, back to back):", "",
+              "| attention kernel | steps | attention us | gap us | decode rows us | gap us | selection us | "
+              "first start to last end us |", "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for k, v in steps.items():
+        m = np.median(np.array(v), axis=0)
+        lines.append(f"| `{k}` | {len(v)} | " + " | ".join(f"{x:.2f}" for x in m) + " |")
+    # regions in the order the step bench runs them (W warm-up steps, then K
+    # plain, K with the phase ring, K warm, and the back-to-back region)
+    W, K = args.warmup, args.steps
+    regions = [("warm-up", W), ("plain (headline)", K), ("phase ring (roofline)", K), ("warm", K),
+               ("back to back", None)]
+    lines += ["", f"Per region (mean us per launch; regions by launch order for --warmup {W} --steps {K}):", "",
+              "| attention kernel | region | steps | attention | decode rows | selection |",
+              "|---|---|---:|---:|---:|---:|"]
+    for k, v in steps.items():
+        v = np.array(v)
+        at = 0
+        for rn, cnt in regions:
+            cnt = len(v) - at if cnt is None else cnt
+            seg = v[at:at + cnt]
+            at += cnt
+            if len(seg):
+                lines.append(f"| `{k}` | {rn} | {len(seg)} | {seg[:, 0].mean():.2f} | {seg[:, 2].mean():.2f} | "
+                             f"{seg[:, 4].mean():.2f} |")
+    lines.append("")
+    fn = os.path.join(ROOT, "profiles", f"{name}_kernel_stats.md")
+    open(fn, "w").write("\n".join(lines))
+    print("\n".join(lines))
+
+
 class DeviceProvider:
     """Model stand-in for the serving bench: inputs of the right shapes and
     distributions made once on the device (queries, fresh block KV, spiked
@@ -1085,6 +1242,14 @@ def main():
                     help="run one 256 MiB device copy first (the reference kernel for FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs into profiles/traffic_<workload>.md (no GPU needed)")
+    ap.add_argument("--kernel-summary", nargs=2, metavar=("DIR", "NAME"),
+                    help="turn a rocprofv3 --kernel-trace run of `bench.py <--bench-args>` into "
+                         "profiles/NAME_kernel_stats.md (no GPU needed)")
+    ap.add_argument("--bench-args", default="", help="--kernel-summary: the arguments the profiled bench run had "
+                                                      "(give as --bench-args=...)")
+    ap.add_argument("--counter-summary", nargs="+", metavar="DIR",
+                    help="turn the rocprofv3 --pmc runs of COUNTER_PASSES into profiles/counters_<workload>.md "
+                         "(no GPU needed)")
     ap.add_argument("--serve", choices=["humaneval-256", "gsm8k-256", "mbpp-512", "truthfulqa-512"],
                     help="closed-loop serving of a table-shaped request stream instead of the step bench")
     ap.add_argument("--serve-requests", type=int, default=256)
@@ -1106,21 +1271,24 @@ def main():
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
-    if args.lm_head and not args.traffic_summary:
+    if args.kernel_summary:
+        kernel_summary(args)
+        return
+    if args.lm_head and not (args.traffic_summary or args.counter_summary):
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
                   file=sys.stderr, flush=True)
             sys.exit(2)
         lm_head_bench(args)
         return
-    if args.config == 5 and not args.traffic_summary and not args.serve:
+    if args.config == 5 and not (args.traffic_summary or args.counter_summary) and not args.serve:
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
                   file=sys.stderr, flush=True)
             sys.exit(2)
         churn_bench(args)
         return
-    if args.refresh and not args.traffic_summary and not args.serve:
+    if args.refresh and not (args.traffic_summary or args.counter_summary) and not args.serve:
         if args.gpus != 1:
             print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",
                   file=sys.stderr, flush=True)
@@ -1134,14 +1302,18 @@ def main():
             sys.exit(2)
         serve_bench(args)
         return
-    if args.traffic_summary:
+    if args.traffic_summary or args.counter_summary:
         import synth
         name = synth.workload(args.config, block_length=args.block_length).name
         if args.lm_head:
             name += f"-lm-head-d{synth.LM_HEAD_DIM[args.config]}"
         if args.refresh:
             name += "-refresh"
-        traffic_summary(args, name + ("-prefix-only" if args.prefix_only else ""))
+        name += "-prefix-only" if args.prefix_only else ""
+        if args.traffic_summary:
+            traffic_summary(args, name)
+        else:
+            counter_summary(args, name)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the step runs on a single device (run with --gpus 1)",

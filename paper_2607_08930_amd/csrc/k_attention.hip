@@ -257,7 +257,8 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   // the cache slot [off + s, off + s + B) straight from LDS, so they are read
   // from memory once. A store counts in vmcnt like the DMA, so a store issued
   // in the loop would make the next stage wait drain it too: the stores come
-  // from the waves that issue no DMA (when the group has any). The
+  // from the waves that issue no DMA (when the group has any); they are
+  // non-temporal whole rows, like the output below. The
   // single-wave loop stores the rows after its last wait instead (measured
   // faster there than holding them in registers through the loop). Only the
   // row-block-0 workgroup of an item stores them.
@@ -279,7 +280,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       for (int cid = gt; cid < nc; cid += gth) {
         const int row = r0 + cid / NCH, c = cid % NCH;
         const v4u v = *reinterpret_cast<const v4u*>(src + row * D + ((c ^ swz<NCH>(row)) * 8));
-        st16(dst + (int64_t)(tb + row) * D + c * 8, v);
+        __builtin_nontemporal_store(v, reinterpret_cast<v4u*>(dst + (int64_t)(tb + row) * D + c * 8));
       }
     }
   };

@@ -38,6 +38,21 @@ __device__ inline void dma16_sv(uint32_t lds, uint64_t base, uint32_t off) {
                : "memory");
 }
 
+// The same two transfers with the non-temporal hint: for tiles read exactly
+// once (the step attention's K/V stream), so they do not displace lines that
+// other work reuses. Kernels that share tiles through L2 (the output head,
+// the refresh) use the plain forms.
+__device__ inline void dma16_once(uint32_t lds, const void* gptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(gptr)
+               : "memory");
+}
+__device__ inline void dma16_sv_once(uint32_t lds, uint64_t base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(off), "s"(uniform64(reinterpret_cast<const void*>(base)))
+               : "memory");
+}
+
 // Wait until at most N (compile time) of this wave's vector-memory operations
 // are outstanding. gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] |
 // vmcnt_hi[15:14]; counts above 63 wait for everything.

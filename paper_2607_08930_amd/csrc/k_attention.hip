@@ -134,7 +134,9 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a, int jblocks) {
 // of one feature: two of them form the 8-key A operand of O^T += V^T P^T.
 // The DMA is issued through inline assembly and waited for with explicit
 // vmcnt counts: the compiler's waitcnt pass cannot see it, and would otherwise
-// drain every stage in flight before reading the current one.
+// drain every stage in flight before reading the current one. The K/V tiles
+// are read once, with the non-temporal hint (measured: LLaDA-8B layer
+// attention 60.4 -> 57.3 us).
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4;
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -221,7 +223,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       for (int k = 0; k < PB; ++k) {
         const int tensor = k / RPI, r = k % RPI;
         const int row = row_of(r);
-        dma16_sv(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), tensor ? vb : kb,
+        dma16_sv_once(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), tensor ? vb : kb,
                  (uint32_t)(row * D + chunk_of(row) * 8) * 2u);
       }
     } else {
@@ -234,7 +236,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
         const bool fresh = (t >= bs) & (t < be);
         const uint16_t* src = tensor ? (fresh ? vnb + (int64_t)(t - bs) * fstride : vcb + (int64_t)t * D)
                                      : (fresh ? knb + (int64_t)(t - bs) * fstride : kcb + (int64_t)t * D);
-        dma16(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), src + chunk_of(row) * 8);
+        dma16_once(sbase + (uint32_t)((tensor * TILE + r * NI * RPB * D) * 2), src + chunk_of(row) * 8);
       }
     }
   };

@@ -69,7 +69,9 @@ struct Lanes<float> {
   __device__ static inline void mask(v4u& v, int e, bool drop) { v[e] = drop ? 0xFF800000u : v[e]; }
 };
 
-// Loads of one chunk: vector u of thread tid starts at element v0 + (u*256 + tid)*N.
+// Loads of one chunk: vector u of thread tid starts at element v0 + (u*256 + tid)*N,
+// with the non-temporal hint (a logits row is read once; measured: Dream-7B
+// layer decode rows 56.6 -> 54.6 us).
 // A vector that starts past the row end re-reads the chunk's first vector (a
 // valid address); elements at or past V are masked when the chunk is folded.
 // A vector starting before V stays inside the row's padded 16-byte stride.
@@ -79,7 +81,7 @@ __device__ inline void load_chunk(v4u (&buf)[kLoads], const T* x, int v0, int V,
 #pragma unroll
   for (int u = 0; u < kLoads; ++u) {
     const int e = v0 + (u * kThreads + tid) * N;
-    buf[u] = ld16(x + (e < V ? e : v0));
+    buf[u] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(x + (e < V ? e : v0)));
   }
 }
 

@@ -350,16 +350,22 @@ def traffic_summary(args, workload):
     import glob
 
     def load(d, counter):
-        per = {}
+        per, copies = {}, []
         for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             for r in csv.DictReader(open(fn)):
                 if r["Counter_Name"] == counter:
                     per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
-        return per
+                    if "copyBuffer" in r["Kernel_Name"]:
+                        copies.append((int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+        return per, sorted(copies)
 
-    fetch, write = load(args.traffic_summary[0], "FETCH_SIZE"), load(args.traffic_summary[1], "WRITE_SIZE")
-    cal_f = max(v for k, vs in fetch.items() if "copyBuffer" in k for v in vs)
-    cal_w = max(v for k, vs in write.items() if "copyBuffer" in k for v in vs)
+    (fetch, fcop), (write, wcop) = load(args.traffic_summary[0], "FETCH_SIZE"), load(args.traffic_summary[1], "WRITE_SIZE")
+    # the calibration copy is the first runtime copy of more than 32 MiB (it
+    # runs before any timed region; later copies, such as the bench's copy
+    # reference, can be larger), the same dispatch in both runs
+    cal_id = next(i for i, v in fcop if v * 1024 > (32 << 20))
+    cal_f = next(v for i, v in fcop if i == cal_id)
+    cal_w = next(v for i, v in wcop if i == cal_id)
     kf, kw = CALIB_BYTES / (cal_f * 1024), CALIB_BYTES / (cal_w * 1024)
     lines = [f"# Measured HBM traffic per launch: {workload}", "",
              "Commands (repo root as `$R`, one MI355X; the bench adds one 256 MiB device copy as the",
@@ -532,6 +538,8 @@ def kernel_summary(args):
               "|---|---|---:|---:|---:|---:|"]
     for k, v in steps.items():
         v = np.array(v)
+        if len(v) != W + 3 * K + 4 * K:      # not the one-layer bench's region layout
+            continue
         at = 0
         for rn, cnt in regions:
             cnt = len(v) - at if cnt is None else cnt

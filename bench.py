@@ -533,9 +533,7 @@ def kernel_summary(args):
     W, K = args.warmup, args.steps
     regions = [("warm-up", W), ("plain (headline)", K), ("phase ring (roofline)", K), ("warm", K),
                ("back to back", None)]
-    lines += ["", f"Per region (mean us per launch; regions by launch order for --warmup {W} --steps {K}):", "",
-              "| attention kernel | region | steps | attention | decode rows | selection |",
-              "|---|---|---:|---:|---:|---:|"]
+    region_lines = []
     for k, v in steps.items():
         v = np.array(v)
         if len(v) != W + 3 * K + 4 * K:      # not the one-layer bench's region layout
@@ -546,8 +544,12 @@ def kernel_summary(args):
             seg = v[at:at + cnt]
             at += cnt
             if len(seg):
-                lines.append(f"| `{k}` | {rn} | {len(seg)} | {seg[:, 0].mean():.2f} | {seg[:, 2].mean():.2f} | "
-                             f"{seg[:, 4].mean():.2f} |")
+                region_lines.append(f"| `{k}` | {rn} | {len(seg)} | {seg[:, 0].mean():.2f} | "
+                                    f"{seg[:, 2].mean():.2f} | {seg[:, 4].mean():.2f} |")
+    if region_lines:
+        lines += ["", f"Per region (mean us per launch; regions by launch order for --warmup {W} --steps {K}):", "",
+                  "| attention kernel | region | steps | attention | decode rows | selection |",
+                  "|---|---|---:|---:|---:|---:|"] + region_lines
     lines.append("")
     fn = os.path.join(ROOT, "profiles", f"{name}_kernel_stats.md")
     open(fn, "w").write("\n".join(lines))

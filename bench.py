@@ -371,7 +371,7 @@ def traffic_summary(args, workload):
              "Commands (repo root as `$R`, one MI355X; the bench adds one 256 MiB device copy as the",
              "calibration kernel):", "", "```", "cd /tmp && export TMPDIR=/tmp"]
     mode = " --lm-head" if args.lm_head else (" --refresh" if args.refresh else "")
-    for c, d in (("FETCH_SIZE", args.traffic_summary[0]), ("WRITE_SIZE", args.traffic_summary[1])):
+    for c, d in (("FETCH_SIZE", "<fetch dir>"), ("WRITE_SIZE", "<write dir>")):
         lines.append(f"rocprofv3 --pmc {c} -d {d} -o run --output-format csv -- "
                      f"python3 $R/bench.py{mode} --config {args.config} --steps 5 --warmup 1 --no-cpu-baseline --pmc-calibration")
     lines += [f"python3 $R/bench.py{mode} --config {args.config} --traffic-summary <fetch dir> <write dir>", "```", "",

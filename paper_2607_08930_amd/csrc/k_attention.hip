@@ -260,9 +260,10 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
   // from memory once. A store counts in vmcnt like the DMA, so a store issued
   // in the loop would make the next stage wait drain it too: the stores come
   // from the waves that issue no DMA (when the group has any); they are
-  // non-temporal whole rows, like the output below. The
-  // single-wave loop stores the rows after its last wait instead (measured
-  // faster there than holding them in registers through the loop). Only the
+  // non-temporal whole rows, like the output below. The single-wave loop
+  // issues them itself, as plain stores, and counts them in its waits: a wait
+  // two tiles later covers them, and non-temporal stores were measured to
+  // hold that wait up (LLaDA-8B layer attention 57.0 -> 60.7 us). Only the
   // row-block-0 workgroup of an item stores them.
   const bool do_wb = a.write_back && it.rb == 0;
   uint16_t* kcw = static_cast<uint16_t*>(a.k_cache) + cache_off;
@@ -424,12 +425,33 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       write_back_tile(ring + (tile % NS) * STAGE, tb);
     }
   } else {
+    // The fresh block rows a tile holds are stored from the LDS tile after
+    // the tile is consumed, always as SPT full store instructions per tensor
+    // (a lane whose row lies outside the block stores a block row's chunk
+    // again, the same bytes to the same address), so the next tile's wait
+    // knows how many vmcnt entries the stores add behind its stage: with two
+    // stages, stage t + 1 is issued before tile t's stores and stage t + 2
+    // after them.
+    static_assert(NS == 2, "the store count in the waits assumes one stage ahead");
+    constexpr int SPT = KT * NCH / 64;
+    bool stored = false;                          // the previous tile issued 2 SPT stores
     for (int tile = 0; tile < ntiles; ++tile) {
       const int nxt = tile + NS - 1;
-      if (nxt < ntiles) issue(nxt % NS, nxt * KT);
-      // this tile's stage has landed once only the later stages' DMAs remain
-      // (a single wave issues all 2 * BPT blocks of a stage)
-      wait_stages(min(NS - 1, ntiles - tile - 1));
+      const bool ahead = nxt < ntiles;
+      if (ahead) issue(nxt % NS, nxt * KT);
+      // this tile's stage has landed once only the next stage's DMA (if
+      // issued) and the previous tile's stores (if any) remain
+      if (ahead) {
+        if (stored)
+          wait_vm_c<PB + 2 * SPT>();
+        else
+          wait_vm_c<PB>();
+      } else {
+        if (stored)
+          wait_vm_c<2 * SPT>();
+        else
+          wait_vm_c<0>();
+      }
       const uint16_t* kt = ring + (tile % NS) * STAGE;
       const uint16_t* vtl = kt + TILE;
       const int tb = tile * KT;
@@ -491,36 +513,29 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem& it, uint16_t
       }
       // the wave consumed its LDS reads through the MFMAs above before its
       // next issue overwrites the slot
-    }
-  }
-  const float lt = lsum + __shfl_xor(lsum, 32, 64);
-  // single-wave loop: the in-place KV update after the last wait (the rows
-  // are read again, from k_new / v_new, and stored into the cache slot)
-  if constexpr (!SHARED) {
-    if (do_wb) {
-      constexpr int MAXWB = 32 * D / 8 / 64;          // 16-byte chunks per lane for a 32-row block
-      const int nch = it.B * (D / 8);
-      for (int base = 0; base < nch; base += 64 * MAXWB) {
-        v4u kw[MAXWB], vw[MAXWB];
+      stored = do_wb && tb < be && tb + KT > bs;
+      if (stored) {
+        // every LDS read first, then the stores (one LDS latency, not 2 SPT)
+        const int r0 = max(bs, tb) - tb, r1 = min(be, tb + KT) - tb;
+        v4u wv[2][SPT];
+        int wrow[SPT];
 #pragma unroll
-        for (int u = 0; u < MAXWB; ++u) {
-          const int cid = min(base + lane + u * 64, nch - 1);
-          const int64_t src = (int64_t)(cid / (D / 8)) * fstride + (cid % (D / 8)) * 8;
-          kw[u] = ld16(knb + src);
-          vw[u] = ld16(vnb + src);
-        }
+        for (int k = 0; k < SPT; ++k) wrow[k] = min(max(k * (64 / NCH) + lane / NCH, r0), r1 - 1);
+        const int c = lane % NCH;
 #pragma unroll
-        for (int u = 0; u < MAXWB; ++u) {
-          const int cid = base + lane + u * 64;
-          if (cid < nch) {
-            const int64_t dst = (int64_t)(bs + cid / (D / 8)) * D + (cid % (D / 8)) * 8;
-            st16(kcw + dst, kw[u]);
-            st16(vcw + dst, vw[u]);
-          }
-        }
+        for (int tensor = 0; tensor < 2; ++tensor)
+#pragma unroll
+          for (int k = 0; k < SPT; ++k)
+            wv[tensor][k] = *reinterpret_cast<const v4u*>(kt + tensor * TILE + wrow[k] * D + ((c ^ swz<NCH>(wrow[k])) * 8));
+#pragma unroll
+        for (int tensor = 0; tensor < 2; ++tensor)
+#pragma unroll
+          for (int k = 0; k < SPT; ++k)
+            st16((tensor ? vcw : kcw) + (int64_t)(tb + wrow[k]) * D + c * 8, wv[tensor][k]);
       }
     }
   }
+  const float lt = lsum + __shfl_xor(lsum, 32, 64);
   // Output: lane (g, n) holds O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4]
   // [query n]. The wave's 32 x D tile is staged row-major in LDS (rows padded
   // by 16 bytes against bank conflicts) and stored as whole rows, 16 bytes per

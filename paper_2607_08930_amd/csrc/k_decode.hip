@@ -24,6 +24,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kLoads = kDecChunkBytes / (kThreads * 16);  // 8
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 // max without the canonicalisation fmaxf needs in IEEE mode: every value
 // reduced here is a finite logit or -inf (masked tail), never NaN
@@ -103,12 +104,15 @@ __device__ inline void mask_tail(v4u (&buf)[kLoads], int v0, int V, int tid) {
 // order: exact max `mt` with the start `vbest` of the first 16-byte vector
 // holding it, and the sum `s` of exp(x - mb / log2 e). The shift mb (log2
 // domain) is raised lazily, only when a vector's max exceeds it by more than
-// 8, so every term stays below 2^8 and the sum far from overflow. mb starts at
-// -FLT_MAX rather than -inf so that -inf elements contribute exp2(-inf) = 0.
+// 8, so every term stays below 2^8 and the sum far from overflow; `thr` is
+// that bound in logit units, (mb + 8) ln 2, so the common case costs one
+// compare per vector. mb starts at -FLT_MAX rather than -inf so that -inf
+// elements contribute exp2(-inf) = 0.
 struct RowAcc {
   float mt = -__builtin_inff();
   int vbest = 0;
   float mb = -FLT_MAX;
+  float thr = -FLT_MAX;
   float s = 0.0f;
 };
 
@@ -125,14 +129,18 @@ __device__ inline void fold_vector(const v4u& v, int e0, RowAcc& r) {
     r.mt = vm;
     r.vbest = e0;
   }
-  const float nb = vm * kLog2e;
-  if (nb > r.mb + 8.0f) {
+  if (vm > r.thr) {
+    // rare (a handful of times per row): a real branch, not a select, so the
+    // common path does not evaluate the rescale
+    asm volatile("");
+    const float nb = vm * kLog2e;
     r.s *= __builtin_amdgcn_exp2f(r.mb - nb);
     r.mb = nb;
+    r.thr = (nb + 8.0f) * kLn2;
   }
-  float acc = 0.0f;
+  float acc = __builtin_amdgcn_exp2f(fmaf(f[0], kLog2e, -r.mb));
 #pragma unroll
-  for (int k = 0; k < N; ++k) acc += __builtin_amdgcn_exp2f(fmaf(f[k], kLog2e, -r.mb));
+  for (int k = 1; k < N; ++k) acc += __builtin_amdgcn_exp2f(fmaf(f[k], kLog2e, -r.mb));
   r.s += acc;
 }
 

@@ -273,6 +273,30 @@ def source_hash(kernel):
     return h.hexdigest()[:16]
 
 
+def measured_hashes(dirs):
+    """Source hashes a --pmc-calibration bench run printed into the log kept
+    beside its profiler output directory (<dir>.log), or None when no log
+    holds them; every directory given must agree."""
+    found = None
+    for d in dirs:
+        fn = d.rstrip("/") + ".log"
+        if not os.path.exists(fn):
+            return None
+        got = None
+        for line in open(fn, errors="replace"):
+            if line.startswith("[bench] source hashes "):
+                got = json.loads(line[len("[bench] source hashes "):])
+        if got is None or (found is not None and got != found):
+            return None
+        found = got
+    return found
+
+
+def hash_note(measured):
+    return ("hash of the kernel's sources in the measured run" if measured is not None else
+            "hash of the kernel's sources when this summary was written (the run's log did not record it)")
+
+
 def traffic_file(workload):
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
 
@@ -380,6 +404,7 @@ def traffic_summary(args, workload):
               "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | read bytes | written bytes | total bytes |",
               "|---|---:|---:|---:|---:|---:|---:|"]
     keep = []
+    hashes = measured_hashes(args.traffic_summary)
     for name in sorted(set(fetch) & set(write)):
         short = name.replace("void ", "").replace("bs::(anonymous namespace)::", "").split("(")[0]
         pref = next((k for k in KERNEL_SOURCES if short.startswith(k)), None)
@@ -388,8 +413,9 @@ def traffic_summary(args, workload):
         f_ = float(np.mean(fetch[name])); w_ = float(np.mean(write[name]))
         rd, wr = f_ * 1024 * kf, w_ * 1024 * kw
         lines.append(f"| `{short}` | {len(fetch[name])} | {f_:.0f} | {w_:.0f} | {rd:.0f} | {wr:.0f} | {rd + wr:.0f} |")
-        keep.append(f"`traffic {pref} {int(round(rd + wr))} {source_hash(pref)}`")
-    lines += ["", "Machine-readable (kernel, bytes per launch, hash of the kernel's sources when measured;",
+        hsh = hashes[pref] if hashes is not None else source_hash(pref)
+        keep.append(f"`traffic {pref} {int(round(rd + wr))} {hsh}`")
+    lines += ["", f"Machine-readable (kernel, bytes per launch, {hash_note(hashes)};",
               "bench.py reports `traffic` only while the hash matches):", ""] + [k + "  " for k in keep] + [""]
     open(traffic_file(workload), "w").write("\n".join(lines))
     print("\n".join(lines))
@@ -421,7 +447,9 @@ def counter_summary(args, workload):
         for fn in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             for r in csv.DictReader(open(fn)):
                 name = r["Kernel_Name"].replace("void ", "").replace("bs::(anonymous namespace)::", "").split("(")[0]
-                if not any(name.startswith(k) for k in KERNEL_SOURCES):
+                if "Cijk_" in name:                  # the library GEMM of the unfused output-head comparison
+                    name = "hipBLASLt GEMM " + next((t for t in name.split("_") if t.startswith("MT")), "")
+                elif not any(name.startswith(k) for k in KERNEL_SOURCES):
                     continue
                 vals.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                 key = (d, r["Dispatch_Id"])
@@ -451,6 +479,7 @@ def counter_summary(args, workload):
               "waits issue | co-issue | MFMA insts | VALU insts | trans. insts | LDS insts |",
               "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     keep = []
+    hashes = measured_hashes(args.counter_summary)
     for name in sorted(vals):
         v = {c: float(np.mean(x)) for c, x in vals[name].items()}
         us = float(np.mean(list(dur[name].values())))
@@ -471,10 +500,11 @@ def counter_summary(args, workload):
         lines.append(f"| `{name}` | {n_disp} | {us:.2f} | {g / us / 1e3:.2f} | {pct(mfma)} | {pct(valu)} | "
                      f"{pct(lds)} | {pct(bc)} | {pct(wa)} | {pct(wi)} | {pct(co)} | {get('SQ_INSTS_MFMA'):.0f} | "
                      f"{get('SQ_INSTS_VALU'):.0f} | {get('SQ_INSTS_VALU_TRANS_F32'):.0f} | {get('SQ_INSTS_LDS'):.0f} |")
-        pref = next(k for k in KERNEL_SOURCES if name.startswith(k))
-        keep.append(f"`counters {pref} {source_hash(pref)}`")
-    lines += ["", "Sources of each kernel when measured (hash; a changed kernel makes the row stale):", ""] + \
-             [k + "  " for k in sorted(set(keep))] + [""]
+        pref = next((k for k in KERNEL_SOURCES if name.startswith(k)), None)
+        if pref is not None:
+            keep.append(f"`counters {pref} {hashes[pref] if hashes is not None else source_hash(pref)}`")
+    lines += ["", f"Sources of each library kernel ({hash_note(hashes)}; a changed kernel makes the row",
+              "stale):", ""] + [k + "  " for k in sorted(set(keep))] + [""]
     open(os.path.join(ROOT, "profiles", f"counters_{workload}.md"), "w").write("\n".join(lines))
     print("\n".join(lines))
 
@@ -1281,6 +1311,10 @@ def main():
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
+    if args.pmc_calibration:
+        # the summaries tie each counter row to the sources that were measured
+        print("[bench] source hashes " + json.dumps({k: source_hash(k) for k in KERNEL_SOURCES}),
+              file=sys.stderr, flush=True)
     if args.kernel_summary:
         kernel_summary(args)
         return

@@ -1143,9 +1143,13 @@ def step_bench(args, cfg):
         one_step()
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps); timing {args.steps}", file=sys.stderr, flush=True)
-    def timed(ring):
+    flags_host = [torch.empty(t.shape, dtype=t.dtype, pin_memory=True) for t in (st.n_unmasked, st.done, st.eos_seen)]
+
+    def timed(ring, flags=False):
         """K steps, each bracketed by HIP events on the step's stream; with
-        ring, the library's phase events are recorded inside every step."""
+        ring, the library's phase events are recorded inside every step; with
+        flags, each step ends with the copy of its completion flags to pinned
+        host memory (what a serving loop reads before its next step)."""
         evs = [region_events() for _ in range(args.steps)]
         if ring:
             bs.bs_profile_begin(ctx, args.steps)
@@ -1155,6 +1159,10 @@ def step_bench(args, cfg):
             reset()
             evs[k][0].record(stream)
             one_step()
+            if flags:
+                with torch.cuda.stream(stream):
+                    for h, d in zip(flags_host, (st.n_unmasked, st.done, st.eos_seen)):
+                        h.copy_(d, non_blocking=True)
             evs[k][1].record(stream)
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) / args.steps * 1e3
@@ -1170,6 +1178,8 @@ def step_bench(args, cfg):
     sweep[0] = False
     warm_ms, _, _ = timed(False)
     sweep[0] = not args.warm
+    # the same steps, each ending with its completion flags copied to the host
+    flag_ms, _, _ = timed(False, flags=True)
     # back to back: K steps between one pair of events, as a serving loop
     # runs them. Step k reads input set k % NB (copies of the layer inputs
     # and logits at other addresses, so a set was last read NB - 1 steps and
@@ -1227,6 +1237,7 @@ def step_bench(args, cfg):
                 "frac_of_peak": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                 "frac_of_copy_reference": round(copy_ms / ms, 4)},
         "ms_per_step_warm": round(float(np.median(warm_ms)), 5),
+        "ms_per_step_with_flag_readback": round(float(np.median(flag_ms)), 5),
         "back_to_back": None if b2b is None else {
             "ms_per_step": round(b2b[0], 5), "positions_per_s": round(ab["positions"] / (b2b[0] / 1e3), 1),
             "achieved_GBps": round(step_bytes / (b2b[0] / 1e3) / 1e9, 1),

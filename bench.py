@@ -1384,7 +1384,8 @@ def main():
         res["second_config"] = {k: second[k] for k in ("value", "unit", "ms_per_step", "config", "hbm", "roofline",
                                                        "phases_ms", "kernel_GBps", "attention_tflops",
                                                        "attention_mfma_frac", "step_ms_p10_p90", "back_to_back",
-                                                       "ms_per_step_warm", "copy_reference", "parity", "cpu_baseline")
+                                                       "ms_per_step_warm", "ms_per_step_with_flag_readback", "copy_reference",
+                                                       "parity", "cpu_baseline")
                                 if k in second}
     print(json.dumps(res), flush=True)
 

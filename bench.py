@@ -551,10 +551,11 @@ def kernel_summary(args):
     for k in sorted(per, key=lambda k: -sum(per[k])):
         v = per[k]
         lines.append(f"| `{k}` | {len(v)} | {np.mean(v):.2f} | {np.min(v):.2f} | {np.max(v):.2f} |")
-    lines += ["", "Per step (attention launch, then the decode row reductions and the selection): median over the",
-              "steps of every timed region of the run (isolated, phase ring, warm, back to back):", "",
-              "| attention kernel | steps | attention us | gap us | decode rows us | gap us | selection us | "
-              "first start to last end us |", "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    if steps:
+        lines += ["", "Per step (attention launch, then the decode row reductions and the selection): median over the",
+                  "steps of every timed region of the run (isolated, phase ring, warm, back to back):", "",
+                  "| attention kernel | steps | attention us | gap us | decode rows us | gap us | selection us | "
+                  "first start to last end us |", "|---|---:|---:|---:|---:|---:|---:|---:|"]
     for k, v in steps.items():
         m = np.median(np.array(v), axis=0)
         lines.append(f"| `{k}` | {len(v)} | " + " | ".join(f"{x:.2f}" for x in m) + " |")

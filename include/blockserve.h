@@ -214,8 +214,9 @@ int bs_dual_cache_block_attention(bs_ctx* ctx, const bs_req_desc* reqs, int n, i
  * any position is masked); L <= 64.
  * ws: device workspace of at least bs_decode_workspace_bytes(...) bytes,
  * 16-byte aligned; its contents on entry are ignored (it carries per-row
- * partial results between the call's two launches). Calls that may overlap
- * (different streams) need different workspaces.
+ * partial results between the call's two launches, and in the fused step
+ * each request's block mask bits from its attention to its decode). Calls
+ * that may overlap (different streams) need different workspaces.
  */
 size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype logits_dt);
 int bs_parallel_decode(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int V,

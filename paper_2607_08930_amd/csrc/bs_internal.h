@@ -61,6 +61,12 @@ struct AttnArgs {
   void* v_cache;
   void* out;
   int write_back;
+  // NULL, or where one item per request (KV head 0, first row block) stores
+  // the request's block mask word, read from `masked` (dense [R][W] box with
+  // row stride msk_rs) for the row reductions that follow
+  uint64_t* mask_words;
+  const uint8_t* masked;
+  int64_t msk_rs;
 };
 
 constexpr int kMhaWaves = 4;  // waves (independent items) per workgroup of the single-wave bf16 kernel
@@ -85,8 +91,11 @@ inline int dec_parts(int V, int eb) {
   return (int)((chunks + kDecPartChunks - 1) / kDecPartChunks);
 }
 
-// Decode workspace: [n * L * parts] DecPartial part results.
-inline size_t dec_workspace_bytes(int n, int L, int parts) { return (size_t)n * L * parts * sizeof(DecPartial); }
+// Decode workspace: [n * L * parts] DecPartial part results, then [n] block
+// mask words (bit j of word i: block position j of request i is masked; set
+// by the fused step's attention, read by its row reductions).
+inline size_t dec_parts_bytes(int n, int L, int parts) { return (size_t)n * L * parts * sizeof(DecPartial); }
+inline size_t dec_workspace_bytes(int n, int L, int parts) { return dec_parts_bytes(n, L, parts) + (size_t)n * 8; }
 
 struct DecArgs {
   const bs_req_desc* reqs;
@@ -109,6 +118,10 @@ struct DecArgs {
   int dense;
   int64_t tok_rs, msk_rs;
   int32_t* pos_out;  // [n][L] or NULL: s_i + j for j < B_i, else -1
+  // NULL, or the block mask words of the requests (see dec_workspace_bytes):
+  // the row reductions then walk a grid ordered by the k-th masked position
+  // of each request and skip the descriptor and mask reads
+  const uint64_t* words;
 };
 
 hipError_t launch_decode(const DecArgs& a, bs_dtype dt, hipStream_t s);

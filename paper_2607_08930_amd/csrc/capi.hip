@@ -993,8 +993,15 @@ static hipError_t step_launch(bs_ctx* c, const void* dblob, const int* meta, int
                               int32_t* pos_out, void* ws, hipStream_t s) {
   hipError_t e = prof_mark(c, 0, s);
   AttnArgs a = attention_args(dblob, meta, L, Hq, Hkv, D, R, W, scale, write_back);
+  // the bf16 attention of the first layer also leaves each request's block
+  // mask word behind the decode partials, for the row reductions below
+  const int parts = dec_parts(V, dtype_bytes(logits_dt));
+  uint64_t* words = reinterpret_cast<uint64_t*>(static_cast<unsigned char*>(ws) + dec_parts_bytes(n, L, parts));
+  const bool use_words = n_layers > 0 && dt == BS_BF16;
   for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
     a.q = q[l]; a.k_new = k_new[l]; a.v_new = v_new[l]; a.k_cache = k_cache[l]; a.v_cache = v_cache[l]; a.out = out[l];
+    a.mask_words = use_words && l == 0 ? words : nullptr;
+    a.masked = masked; a.msk_rs = masked_row_stride;
     e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
   }
   if (e == hipSuccess) e = prof_mark(c, 1, s);
@@ -1004,6 +1011,7 @@ static hipError_t step_launch(bs_ctx* c, const void* dblob, const int* meta, int
     d.tokens = tokens; d.masked = masked;
     d.dense = 1; d.tok_rs = tokens_row_stride; d.msk_rs = masked_row_stride;
     d.pos_out = pos_out;
+    d.words = use_words ? words : nullptr;
     e = launch_decode_marked(d, logits_dt, s, [&](int ph) { return prof_mark(c, ph, s); });
   }
   if (e == hipSuccess && c->prof.on && c->prof.used < c->prof.cap) ++c->prof.used;

@@ -293,6 +293,17 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     }
   };
   const int ntiles = (len + KT - 1) / KT;
+  // The request's block mask word, in the fused step (one item per request:
+  // KV head 0, first row block, its first wave): lane j reads mask cell j of
+  // the block, by inline assembly so the compiler adds no wait of its own;
+  // issued before the DMA, so every later wait of this wave covers it, and
+  // consumed after the last one.
+  const bool word_owner = a.mask_words != nullptr && it.kvh == 0 && it.rb == 0 && wg == 0;
+  uint32_t mcell = 0;
+  if (word_owner) {
+    const uint8_t* mp = a.masked + it.row * a.msk_rs + it.off + it.s + (lane < it.B ? lane : 0);
+    asm volatile("global_load_ubyte %0, %1, off" : "=v"(mcell) : "v"(mp) : "memory");
+  }
   // prologue: stages 0 .. NS-2 (issued before anything else so the first
   // tiles are in flight while the queries load)
   if (issuer) {
@@ -579,6 +590,12 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
         __builtin_nontemporal_store(v, reinterpret_cast<v4u*>(op + c * 8));
       }
     }
+  }
+  if (word_owner) {
+    wait_vm_c<0>();
+    asm volatile("" : "+v"(mcell));                 // read only after the wait
+    const uint64_t bits = __ballot(lane < it.B && mcell != 0);
+    if (lane == 0) a.mask_words[it.req] = bits;
   }
 }
 

@@ -257,11 +257,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   constexpr int N = Lanes<T>::N;
   constexpr int CH = kDecChunkBytes / sizeof(T);
   static_assert(kDecPartChunks >= 1 && kDecPartChunks <= 4, "stream_part is instantiated for 1..4 chunks");
-  const int row = blockIdx.x / a.parts, part = blockIdx.x - row * a.parts;
-  const int i = row / a.L, j = row - i * a.L;
-  const bs_req_desc rq = a.reqs[i];
-  const Geo q = geo_of(rq, a.L);
-  if (j >= q.B || a.masked[state_cell(a, rq, q, i, j, a.msk_rs)] == 0) return;
+  int row, part;
+  if (a.words) {
+    // fused step: workgroup (k, i, part), k outermost, streams part `part` of
+    // the k-th masked position of request i; k past the request's count exits
+    // (those workgroups come last in the grid)
+    const int t = blockIdx.x / a.parts;
+    part = blockIdx.x - t * a.parts;
+    const int k = t / a.n, i = t - k * a.n;
+    uint64_t bits = a.words[i];
+    if (k >= __popcll(bits)) return;
+    for (int r = 0; r < k; ++r) bits &= bits - 1;
+    row = i * a.L + __builtin_ctzll(bits);
+  } else {
+    row = blockIdx.x / a.parts;
+    part = blockIdx.x - row * a.parts;
+    const int i = row / a.L, j = row - i * a.L;
+    const bs_req_desc rq = a.reqs[i];
+    const Geo q = geo_of(rq, a.L);
+    if (j >= q.B || a.masked[state_cell(a, rq, q, i, j, a.msk_rs)] == 0) return;
+  }
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const T* x = static_cast<const T*>(a.logits) + (int64_t)row * a.row_stride;
   const int nchunk = (a.V + CH - 1) / CH;

@@ -91,13 +91,14 @@ def test_lm_head_workspace_query():
 
 def test_workspace_queries():
     # a 126464-entry bf16 row is 8 chunks of 32 KiB, streamed as 4 parts of 2
-    # chunks; the workspace holds one 16-byte part result per (i, j, part)
-    assert bs.bs_decode_workspace_bytes(32, 32, 126464, bs.BS_BF16) == 32 * 32 * 4 * 16
-    assert bs.bs_decode_workspace_bytes(2, 4, 16384, bs.BS_BF16) == 2 * 4 * 16       # exactly one chunk
-    assert bs.bs_decode_workspace_bytes(2, 4, 16385, bs.BS_BF16) == 2 * 4 * 16       # two chunks, one part
-    assert bs.bs_decode_workspace_bytes(2, 4, 32769, bs.BS_BF16) == 2 * 4 * 2 * 16   # three chunks
-    assert bs.bs_decode_workspace_bytes(4, 8, 1000, bs.BS_F32) == 4 * 8 * 16
-    assert bs.bs_decode_workspace_bytes(3, 5, 1000, bs.BS_F32) == 3 * 5 * 16
+    # chunks; the workspace holds one 16-byte part result per (i, j, part),
+    # then one 8-byte block mask word per request
+    assert bs.bs_decode_workspace_bytes(32, 32, 126464, bs.BS_BF16) == 32 * 32 * 4 * 16 + 32 * 8
+    assert bs.bs_decode_workspace_bytes(2, 4, 16384, bs.BS_BF16) == 2 * 4 * 16 + 2 * 8      # exactly one chunk
+    assert bs.bs_decode_workspace_bytes(2, 4, 16385, bs.BS_BF16) == 2 * 4 * 16 + 2 * 8      # two chunks, one part
+    assert bs.bs_decode_workspace_bytes(2, 4, 32769, bs.BS_BF16) == 2 * 4 * 2 * 16 + 2 * 8  # three chunks
+    assert bs.bs_decode_workspace_bytes(4, 8, 1000, bs.BS_F32) == 4 * 8 * 16 + 4 * 8
+    assert bs.bs_decode_workspace_bytes(3, 5, 1000, bs.BS_F32) == 3 * 5 * 16 + 3 * 8
     assert bs.bs_decode_workspace_bytes(0, 8, 1000, bs.BS_F32) == 0
     reqs = np.array([(5, 16, 1, 0, 31)], bs.REQ_DTYPE)
     assert bs.bs_attention_workspace_bytes(reqs, 8, 2, 2, 64, bs.BS_F32) >= 0

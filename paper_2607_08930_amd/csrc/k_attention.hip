@@ -183,6 +183,12 @@ __device__ inline int swz(int row) {
 // so fields read through a reference would be loaded again after every issue,
 // as vector loads whose waits also drain the DMA in flight (measured: 2.6 us
 // of the skewed Dream-7B batch's attention).
+// compile-time flag passed to a generic lambda
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
 template <int D, int KT, int NS, bool SHARED, int NI, int I0>
 __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t* ring, int GW, int wg,
                                  int lane) {
@@ -349,64 +355,44 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     for (int rr = 0; rr < 16; ++rr) o[dt][rr] = 0.0f;
   float mrun = -__builtin_inff(), lsum = 0.0f;
   if constexpr (SHARED) {
-    static_assert(KT == 64 && NS >= 3, "the pipelined group loop keeps two 64-key tiles resident");
-    // Software pipeline: iteration t turns tile t's scores (computed in
-    // iteration t - 1) into probabilities and accumulates P V while the score
-    // MFMAs of tile t + 1 run, so the VALU and matrix pipes overlap inside the
-    // wave. Tiles t and t + 1 are resident; t + 2 .. t + NS - 1 are in flight.
-    auto scores = [&](const uint16_t* kt, f32x16_t& s0, f32x16_t& s1) {
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        s0[rr] = 0.0f;
-        s1[rr] = 0.0f;
-      }
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8_t k0 = *reinterpret_cast<const bf16x8_t*>(kt + koff[kk]);
-        const bf16x8_t k1 = *reinterpret_cast<const bf16x8_t*>(kt + 32 * D + koff[kk]);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[kk], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[kk], s1, 0, 0, 0);
-      }
+    static_assert(KT == 64 && NS == 4, "the group loop refills the slot of tile t - 1 while tiles t .. t + 2 are held");
+    // Software pipeline over 64-key tiles, two MFMA blocks per tile, each
+    // interleaved with the VALU work of the same wave (a wave's MFMAs overlap
+    // only its own VALU work), in an order fixed by scheduling fences:
+    //   block 1: P V of tile t - 1 (16 MFMAs) beside the max of tile t's
+    //            scores, the rescale decision, the scaled scores and half of
+    //            the exponentials;
+    //   barrier: tile t + 1 resident, every wave done with tile t - 1, whose
+    //            slot is refilled with tile t + 3;
+    //   block 2: scores of tile t + 1 (16 MFMAs) beside the other
+    //            exponentials, their bf16 conversion and the row sums.
+    // the value is computed here: keeps the compiler from sinking it past the
+    // scheduling fences into the block that uses it
+    auto pin = [](float& x) { asm volatile("" : "+v"(x)); };
+    const float sl2e = a.scale_log2e;
+    f32x16_t sa, sb;           // scores of tile t (keys 0..31 and 32..63 of the tile)
+    float ex[32];              // tile t: scaled scores, then their exponentials
+    bf16x8_t pp[2][2];         // probabilities of the last converted tile: [half][ks]
+    constexpr int NSC = 2 * NKK, NPV = 4 * NDT;   // score and P V MFMAs per tile
+    auto kread = [&](const uint16_t* kt, int j) -> bf16x8_t {   // A operand of score MFMA j
+      return *reinterpret_cast<const bf16x8_t*>(kt + (j & 1) * 32 * D + koff[j >> 1]);
     };
-    auto probs = [&](const f32x16_t& sc, bf16x8_t& p0, bf16x8_t& p1) {
-      const float nm = -mrun;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[rr], a.scale_log2e, nm));
-        if (rr < 8)
-          p0[rr] = (__bf16)pv;
-        else
-          p1[rr - 8] = (__bf16)pv;
-      }
-      lsum = add_weights(add_weights(lsum, p0), p1);
+    auto vread = [&](const uint16_t* vt, int i) -> bf16x8_t {   // A operand of P V MFMA i
+      const int dt = i % NDT, ks = (i / NDT) & 1, hh = i / (2 * NDT);
+      const uint16_t* vs = vt + hh * 32 * D;
+      const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
+      const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     };
-    auto pv = [&](const uint16_t* vs, const bf16x8_t& p0, const bf16x8_t& p1) {
+    auto sfrag = [&](int j) -> f32x16_t& { return (j & 1) ? sb : sa; };
+    // P V of one tile, no interleaving (the tile after the loop)
+    auto pv_plain = [&](const uint16_t* vt) {
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
-          const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
-          const bf16x8_t va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, ks ? p1 : p0, o[dt], 0, 0, 0);
-        }
+      for (int i = 0; i < NPV; ++i)
+        o[i % NDT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(vt, i), pp[i / (2 * NDT)][(i / NDT) & 1],
+                                                            o[i % NDT], 0, 0, 0);
     };
-
-    // tile 0 resident (the later prologue stages may still be in flight)
-    if (issuer) wait_stages(min(ntiles - 1, NS - 2));
-    __syncthreads();
-    f32x16_t sa, sb;
-    scores(ring, sa, sb);
-    for (int tile = 0; tile < ntiles; ++tile) {
-      if (tile + 1 < ntiles) {
-        // tile + 1 landed (stages up to tile + NS - 2 were issued); after the
-        // barrier every wave is done with tile - 1, whose slot is refilled
-        if (issuer) wait_stages(min(ntiles - 1, tile + NS - 2) - tile - 1);
-        __syncthreads();
-        const int nxt = tile + NS - 1;
-        if (issuer && nxt < ntiles) issue(nxt % NS, nxt * KT);
-      }
-      const int tb = tile * KT;
+    auto mask_ragged = [&](int tb) {
       if (tb + KT > len) {                         // ragged last tile only
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
@@ -415,31 +401,136 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
           if (key + 32 >= len) sb[rr] = -__builtin_inff();
         }
       }
-      float mx = vmax(sa[0], sb[0]);
+    };
+
+    // tile 0 resident (the later prologue stages may still be in flight)
+    if (issuer) wait_stages(min(ntiles - 1, NS - 2));
+    __syncthreads();
 #pragma unroll
-      for (int rr = 1; rr < 16; ++rr) mx = vmax(mx, vmax(sa[rr], sb[rr]));
-      mx = vmax(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
-      if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {         // lazy rescale, as below
-        const float mnew = fmaxf(mrun, mx);
-        const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
-        lsum *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-          for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
-        mrun = mnew;
-      }
-      bf16x8_t pa0, pa1, pb0, pb1;
-      probs(sa, pa0, pa1);
-      probs(sb, pb0, pb1);
-      // scores of tile + 1 (on the last tile they read a resident slot and are
-      // discarded), independent of the probabilities above
-      scores(ring + ((tile + 1) % NS) * STAGE, sa, sb);
-      const uint16_t* vt = ring + (tile % NS) * STAGE + TILE;
-      pv(vt, pa0, pa1);
-      pv(vt + 32 * D, pb0, pb1);
-      write_back_tile(ring + (tile % NS) * STAGE, tb);
+    for (int rr = 0; rr < 16; ++rr) {
+      sa[rr] = 0.0f;
+      sb[rr] = 0.0f;
     }
+#pragma unroll
+    for (int j = 0; j < NSC; ++j)
+      sfrag(j) = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kread(ring, j), qb[j >> 1], sfrag(j), 0, 0, 0);
+
+    auto body = [&](auto first_tag, int tile) {
+      constexpr bool FIRST = decltype(first_tag)::value;
+      const int tb = tile * KT;
+      const uint16_t* vprev = ring + ((tile + NS - 1) % NS) * STAGE + TILE;
+      mask_ragged(tb);
+      // ---- block 1
+      bf16x8_t vf[3];
+      if constexpr (!FIRST) {
+        vf[0] = vread(vprev, 0);
+        vf[1] = vread(vprev, 1);
+      }
+      float m8[8];
+      float mx = 0.0f, alpha = 1.0f;
+      bool resc = false;
+      __builtin_amdgcn_sched_barrier(0);
+      // sixteen slots of VALU work; the NPV MFMAs are spread evenly over them
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if constexpr (!FIRST) {
+          if ((i * NPV) % 16 == 0) {
+            const int m = i * NPV / 16;
+            if (m + 2 < NPV) vf[(m + 2) % 3] = vread(vprev, m + 2);
+            o[m % NDT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[m % 3], pp[m / (2 * NDT)][(m / NDT) & 1],
+                                                                o[m % NDT], 0, 0, 0);
+          }
+        }
+        if (i < 2) {
+#pragma unroll
+          for (int k = 4 * i; k < 4 * i + 4; ++k)
+            m8[k] = vmax(vmax(sa[2 * k], sa[2 * k + 1]), vmax(sb[2 * k], sb[2 * k + 1]));
+        } else if (i == 2) {
+          mx = vmax(vmax(vmax(m8[0], m8[1]), vmax(m8[2], m8[3])), vmax(vmax(m8[4], m8[5]), vmax(m8[6], m8[7])));
+          // lanes l and l ^ 32 hold the two halves of a query's keys
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+          mx = vmax(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * sl2e;    // log2 units
+          pin(mx);
+        } else if (i == 3) {
+          // lazy rescale: keep the reference max until a score exceeds it by
+          // 2^8, so the O accumulators are rescaled a handful of times per row
+          resc = __builtin_amdgcn_ballot_w64(mx > mrun + 8.0f) != 0;
+          const float mnew = resc ? fmaxf(mrun, mx) : mrun;
+          alpha = __builtin_amdgcn_exp2f(mrun - mnew);
+          lsum *= alpha;
+          mrun = mnew;
+        } else if (i < 8) {
+#pragma unroll
+          for (int r = 8 * (i - 4); r < 8 * (i - 4) + 8; ++r) {
+            ex[r] = fmaf(r < 16 ? sa[r] : sb[r - 16], sl2e, -mrun);
+            pin(ex[r]);
+          }
+        } else {
+          ex[2 * (i - 8)] = __builtin_amdgcn_exp2f(ex[2 * (i - 8)]);
+          ex[2 * (i - 8) + 1] = __builtin_amdgcn_exp2f(ex[2 * (i - 8) + 1]);
+          pin(ex[2 * (i - 8)]);
+          pin(ex[2 * (i - 8) + 1]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (!FIRST) {
+        if (resc) {                                // rare: after the P V of tile t - 1
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr) o[dt][rr] *= alpha;
+        }
+      }
+      // ---- barrier: tile + 1 landed (stages up to tile + NS - 2 were
+      // issued); every wave is done with tile - 1, whose slot is refilled
+      if (tile + 1 < ntiles) {
+        if (issuer) wait_stages(min(ntiles - 1, tile + NS - 2) - tile - 1);
+        __syncthreads();
+        const int nxt = tile + NS - 1;
+        if (issuer && nxt < ntiles) issue(nxt % NS, nxt * KT);
+      }
+      // ---- block 2 (on the last tile the scores read a resident slot and
+      // are discarded)
+      const uint16_t* knext = ring + ((tile + 1) % NS) * STAGE;
+      bf16x8_t kf[3];
+      kf[0] = kread(knext, 0);
+      kf[1] = kread(knext, 1);
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        sa[rr] = 0.0f;
+        sb[rr] = 0.0f;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if ((j * NSC) % 16 == 0) {
+          const int m = j * NSC / 16;
+          if (m + 2 < NSC) kf[(m + 2) % 3] = kread(knext, m + 2);
+          sfrag(m) = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[m % 3], qb[m >> 1], sfrag(m), 0, 0, 0);
+        }
+        if (j < 8) {
+          ex[16 + 2 * j] = __builtin_amdgcn_exp2f(ex[16 + 2 * j]);
+          ex[17 + 2 * j] = __builtin_amdgcn_exp2f(ex[17 + 2 * j]);
+          pin(ex[16 + 2 * j]);
+          pin(ex[17 + 2 * j]);
+        } else {
+          // values 4 (j - 8) .. + 3 -> bf16 pairs, and their sum
+          const int v0 = 4 * (j - 8);
+          bf16x8_t& dst = pp[v0 >> 4][(v0 >> 3) & 1];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dst[(v0 & 7) + e] = (__bf16)ex[v0 + e];
+          if ((v0 & 7) == 4) {
+            lsum = add_weights(lsum, dst);
+            pin(lsum);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      write_back_tile(ring + (tile % NS) * STAGE, tb);
+    };
+    if (ntiles > 0) body(Flag<true>{}, 0);
+    for (int tile = 1; tile < ntiles; ++tile) body(Flag<false>{}, tile);
+    pv_plain(ring + ((ntiles + NS - 1) % NS) * STAGE + TILE);
   } else {
     // The fresh block rows a tile holds are stored from the LDS tile after
     // the tile is consumed, always as SPT full store instructions per tensor

@@ -145,6 +145,25 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 // or -inf, so NaN propagation never applies)
 __device__ inline float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
 
+// Combine lane l with lane l ^ 32 (the two key halves of a query column):
+// v_permlane32_swap exchanges the 32-lane halves of two registers in the
+// VALU, with no LDS round trip; both halves combine (low, high) in that order.
+__device__ inline void xhalf(float v, float& lo, float& hi) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(sw[0]);
+  hi = __uint_as_float(sw[1]);
+}
+__device__ inline float xhalf_max(float v) {
+  float lo, hi;
+  xhalf(v, lo, hi);
+  return vmax(lo, hi);
+}
+__device__ inline float xhalf_sum(float v) {
+  float lo, hi;
+  xhalf(v, lo, hi);
+  return lo + hi;
+}
+
 // lsum += sum of the eight bf16 weights in p (the values the P V MFMA uses)
 __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
   const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
@@ -366,8 +385,10 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     //            slot is refilled with tile t + 3;
     //   block 2: scores of tile t + 1 (16 MFMAs) beside the other
     //            exponentials, their bf16 conversion and the row sums.
-    // the value is computed here: keeps the compiler from sinking it past the
-    // scheduling fences into the block that uses it
+    // (16 MFMAs per block at D = 128; 8 at D = 64.)
+
+    // pin(x): x is computed here; keeps the compiler from sinking the
+    // arithmetic past the scheduling fences into the block that uses it
     auto pin = [](float& x) { asm volatile("" : "+v"(x)); };
     const float sl2e = a.scale_log2e;
     f32x16_t sa, sb;           // scores of tile t (keys 0..31 and 32..63 of the tile)
@@ -385,7 +406,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
       return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     };
     auto sfrag = [&](int j) -> f32x16_t& { return (j & 1) ? sb : sa; };
-    // P V of one tile, no interleaving (the tile after the loop)
+    // P V of one tile, no interleaving (the last tile, after the loop)
     auto pv_plain = [&](const uint16_t* vt) {
 #pragma unroll
       for (int i = 0; i < NPV; ++i)
@@ -447,9 +468,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
             m8[k] = vmax(vmax(sa[2 * k], sa[2 * k + 1]), vmax(sb[2 * k], sb[2 * k + 1]));
         } else if (i == 2) {
           mx = vmax(vmax(vmax(m8[0], m8[1]), vmax(m8[2], m8[3])), vmax(vmax(m8[4], m8[5]), vmax(m8[6], m8[7])));
-          // lanes l and l ^ 32 hold the two halves of a query's keys
-          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          mx = vmax(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * sl2e;    // log2 units
+          mx = xhalf_max(mx) * sl2e;              // log2 units
           pin(mx);
         } else if (i == 3) {
           // lazy rescale: keep the reference max until a score exceeds it by
@@ -583,7 +602,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
         float mx = sacc[0];
 #pragma unroll
         for (int rr = 1; rr < 16; ++rr) mx = vmax(mx, sacc[rr]);
-        mx = vmax(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2e;   // log2 units
+        mx = xhalf_max(mx) * a.scale_log2e;      // log2 units
         // lazy rescale: keep the reference max until a score exceeds it by 2^8,
         // so the O accumulators are rescaled a handful of times per row
         if (__builtin_amdgcn_ballot_w64(mx > mrun + 8.0f)) {
@@ -642,7 +661,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
       }
     }
   }
-  const float lt = lsum + __shfl_xor(lsum, 32, 64);
+  const float lt = xhalf_sum(lsum);
   // Output: lane (g, n) holds O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4]
   // [query n]. The wave's 32 x D tile is staged row-major in LDS (rows padded
   // by 16 bytes against bank conflicts) and stored as whole rows, 16 bytes per

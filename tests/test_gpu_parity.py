@@ -367,6 +367,22 @@ def test_attention_edge_geometries(ctx):
         _att(ctx, w, label)
 
 
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 128), (28, 4, 128), (12, 2, 64)])
+def test_attention_group_ring_phases(ctx, Hq, Hkv, D):
+    # the group kernel's loop lags P V one 64-key tile behind the scores and
+    # refills the slot of the lagging tile: rows of 1 to 6 tiles, whole and
+    # ragged, cover every position of the last tile in the 4-slot ring, with
+    # the fresh block in the last tiles (first batch) or the first (second)
+    lens = [1, 33, 63, 64, 65, 127, 128, 129, 191, 192, 193, 255, 256, 257, 320, 383]
+    L = 32
+    at_end = synth.custom(L, Hq, Hkv, D, 10, "bf16", [max(t - L, 0) for t in lens],
+                          [min(t, L) for t in lens], [0] * len(lens), kv_sigma=0.1, q_sigma=3.0)
+    at_start = synth.custom(L, Hq, Hkv, D, 10, "bf16", [0] * len(lens), lens, [0] * len(lens),
+                            kv_sigma=0.1, q_sigma=3.0, variant=1)
+    _att(ctx, at_end, f"G{Hq // Hkv} D{D} block last")
+    _att(ctx, at_start, f"G{Hq // Hkv} D{D} block first")
+
+
 def test_attention_long_rows(ctx):
     # rows far longer than the workloads': 16 384 keys for MHA (512 tiles of a
     # single wave's stream) and 12 000 for a 7-head group, next to short rows

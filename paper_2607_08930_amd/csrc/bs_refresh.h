@@ -7,9 +7,9 @@
 
 namespace bs {
 
-constexpr int kRefQ = 256;     // query positions per workgroup (8 waves x 32)
-constexpr int kRefKT = 64;     // keys per LDS stage
-constexpr int kRefNS = 4;      // LDS stages (4 x 32 KiB of K and V)
+constexpr int kRefQ = 128;     // query positions per workgroup (4 waves x 32)
+constexpr int kRefKT = 32;     // keys per LDS stage
+constexpr int kRefNS = 5;      // LDS stages (5 x 16 KiB of K and V: two workgroups per CU)
 
 // One workgroup: query positions [q0, q0 + kRefQ) of one request row and one
 // query head. row < 0 marks an empty slot of the XCD-ordered grid.

@@ -391,7 +391,7 @@ AttnArgs attention_args(const void* dblob, const int* meta, int L, int Hq, int H
 }
 
 // ---- refresh work list
-// One item per (request, query head, 256-query chunk). Items that read the
+// One item per (request, query head, 128-query chunk). Items that read the
 // same K/V (one request and KV head) stay together on one XCD, so their tiles
 // are shared through that XCD's L2: groups, heaviest first, go to the XCD with
 // the least work so far, and XCD x's queue fills grid slots x, x + 8, ...

@@ -12,11 +12,14 @@
 //                from the token-major projections into the head-major cache.
 //                HBM-bound: every byte is read once and written once.
 // k_refresh_attn full-row attention over the refreshed cache, the queries
-//                rotated as they are loaded. A workgroup of eight waves owns
-//                256 query positions of one head, two waves per SIMD and 32
-//                queries per wave (32x32x16 MFMAs). K/V tiles of 64 keys stream
-//                HBM/L2 -> LDS by direct DMA through a 4-stage ring, two tiles
-//                in flight. Inside a wave the loop is software-pipelined by
+//                rotated as they are loaded. A workgroup of four waves owns
+//                128 query positions of one head, 32 queries per wave
+//                (32x32x16 MFMAs), and two workgroups share a CU (two waves
+//                per SIMD), so one workgroup's prologue (first tiles, queries
+//                and their rotation) runs beside the other's loop. K/V tiles
+//                of 32 keys stream HBM/L2 -> LDS by direct DMA through a
+//                5-stage ring, two tiles in flight. Inside a wave the loop is
+//                software-pipelined by
 //                32-key sub-tiles: while the exponentials of sub-tile u run on
 //                the VALU, the matrix core computes the scores of u + 1 and
 //                accumulates P V of u - 1.
@@ -115,7 +118,7 @@ __device__ inline float add_weights(float lsum, const bf16x8_t& p) {
 // shape); QW = 1 reads twice the LDS bytes per MFMA and fits two waves per
 // SIMD (222 VGPRs), which is what the launch uses.
 template <int D, int QW, int NW>
-__global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void k_refresh_attn(RefArgs a) {
   static_assert(D == 128, "the refresh attention is laid out for D = 128");
   static_assert(NW * QW * 32 == kRefQ, "a workgroup covers kRefQ queries");
   constexpr int KT = kRefKT, NS = kRefNS;
@@ -123,7 +126,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
   constexpr int NDT = D / 32;        // 32-feature output tiles
   constexpr int TILE = KT * D;       // elements of one K (or V) tile
   constexpr int STAGE = 2 * TILE;    // K tile, then V tile
-  constexpr int PB = 32 / NW;        // 1 KiB DMA blocks per stage and wave (32 per stage)
+  constexpr int SPT = KT / 32;       // 32-key sub-tiles per tile
+  constexpr int PB = STAGE * 2 / 1024 / NW;   // 1 KiB DMA blocks per stage and wave
   constexpr int WPT = NW / 2;        // waves per tensor (K, then V)
   __shared__ __align__(1024) uint16_t ring[NS * STAGE];
 
@@ -231,7 +235,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
   bool resc_pend = false;
 
   // K rows of sub-tile u (32 keys) start at element sub_k(u); its V rows at + TILE
-  auto sub_k = [&](int u) { return ((u >> 1) % NS) * STAGE + (u & 1) * 32 * D; };
+  auto sub_k = [&](int u) { return ((u / SPT) % NS) * STAGE + (u % SPT) * 32 * D; };
   auto vfrag = [&](const uint16_t* vs, int dt, int ks) {
     const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][0]));
     const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vs + voff[dt][ks][1]));
@@ -283,10 +287,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_refresh_attn(RefArgs a) {
   auto sub_tile = [&](int u, f32x16_t (&sc)[QW], f32x16_t (&sn)[QW], const bf16x8_t (&pprev)[QW][2],
                       bf16x8_t (&pcur)[QW][2]) {
     const int un = u + 1;
-    if (un < nsub && (un & 1) == 0) {
+    if (un < nsub && un % SPT == 0) {
       // sub-tile un opens tile T: it has landed once only tile T + 1 (if
-      // issued) is in flight; after the barrier tile T - 2 is free for T + 2
-      const int T = un >> 1;
+      // issued) is in flight. Tile T + 2 refills the slot of tile T + 2 - NS;
+      // P V runs one sub-tile behind the scores, so this step still reads V
+      // of sub-tile T SPT - 2, in tile T - ceil(2 / SPT): the refilled tile
+      // must be older than that.
+      static_assert(NS >= 3 + (SPT + 1) / SPT, "ring too short for the lagging P V");
+      const int T = un / SPT;
       if (T + 1 < ntiles)
         wait_vm_c<PB>();
       else

@@ -1,7 +1,7 @@
 """GPU parity of the dual-cache refresh (bs_dual_cache_refresh) against the
 oracle: rotated keys and values scattered into the cache, full-row attention
 with rotated queries. Ragged small shapes (rows of 1 to 600 tokens, several
-256-query chunks and 64-key tiles with ragged tails; MHA, GQA with groups of
+128-query chunks and 32-key tiles with ragged tails; MHA, GQA with groups of
 2 and 7) in full, the LLaDA-8B and Dream-7B layer shapes on sampled requests
 and heads plus whole-box properties, the unrotated case, argument checks.
 
@@ -119,8 +119,8 @@ def test_small_ragged_rows_in_full(ctx, Hq, Hkv, base):
 
 @pytest.mark.parametrize("seed", range(6))
 def test_random_geometries(ctx, seed):
-    # seeded random batches: head grouping, lengths 1..700 (ragged 64-key
-    # tiles and 256-query chunks), row order with unused rows, padding slack,
+    # seeded random batches: head grouping, lengths 1..700 (ragged 32-key
+    # tiles and 128-query chunks), row order with unused rows, padding slack,
     # rotary base; every request against the oracle, nothing else written
     torch, bs, bstep = lazy()
     g_ = np.random.default_rng(7000 + seed)

@@ -185,6 +185,12 @@ __device__ inline int swz(int row) {
   return ((row & 3) << 1) | ((row >> 2) & 1);
 }
 
+// compile-time flag passed to a generic lambda
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
 // One (request, KV head) item processed by GW waves that share its K/V tiles:
 // wave wg of the group serves query head c * G + wg / RBW and rows
 // 32 * (rb + wg % RBW) .. + 32 of the block (RBW row blocks per workgroup,
@@ -202,12 +208,6 @@ __device__ inline int swz(int row) {
 // so fields read through a reference would be loaded again after every issue,
 // as vector loads whose waits also drain the DMA in flight (measured: 2.6 us
 // of the skewed Dream-7B batch's attention).
-// compile-time flag passed to a generic lambda
-template <bool B>
-struct Flag {
-  static constexpr bool value = B;
-};
-
 template <int D, int KT, int NS, bool SHARED, int NI, int I0>
 __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t* ring, int GW, int wg,
                                  int lane) {

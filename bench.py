@@ -920,6 +920,13 @@ def churn_bench(args):
     from paper_2607_08930_amd import step as bstep
 
     torch.cuda.set_device(0)
+    if args.pmc_calibration:
+        # the calibration copy, before any other device copy of the run
+        src_ = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst_ = torch.empty_like(src_)
+        dst_.copy_(src_)
+        torch.cuda.synchronize()
+        del src_, dst_
     w = synth.workload(5)
     tok, msk, _ = synth.gen_state(w)
     plan = synth.churn_plan(w, w.reqs, tok, msk, step=1)          # rewrites tok/msk rows in place

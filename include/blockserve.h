@@ -179,11 +179,34 @@ int bs_scatter_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int 
  * D in {64, 128}, L <= 64 and Hq / Hkv <= 8. All pointers
  * 16-byte aligned. Cache cells outside each request's logical row and the
  * stale block slot are never read (they may hold NaN).
- * ws: device workspace of at least bs_attention_workspace_bytes(...) bytes
- * (NULL allowed when that is 0). Its contents need no initialisation.
+ * ws: NULL, or a device workspace of ws_bytes bytes (contents on entry
+ * ignored). Straggler handling (split-KV; the paper's straggler effect,
+ * Introduction and RQ2): the BS_BF16 kernel with G * ceil(L / 32) >= 2 waves
+ * per row runs one workgroup per CU, so a batch of whole rows lasts as long
+ * as its longest row. bs_attention_workspace_bytes(...) returns the bytes of
+ * partial slots for a plan that cuts the longest rows into pieces of 64-key
+ * tiles (each piece writes its un-normalised output, running max and row sum;
+ * a merge launch combines them by log-sum-exp weights), or 0 when no cut pays
+ * off (balanced rows, MHA with L <= 32, BS_F32, invalid arguments). With
+ * ws_bytes at least that size the call runs the plan, otherwise every row
+ * whole; both agree within rounding (bf16 output). The plan depends only on
+ * the arguments of the size query. Calls that may overlap (different
+ * streams) need different workspaces.
  */
 size_t bs_attention_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
                                     bs_dtype dt);
+/*
+ * Host only (no device work): the BS_BF16 attention's work list for these
+ * arguments, in launch order, as 6 int32 per workgroup: request, KV head,
+ * first 32-row block, first and one-past-last 64-key tile, partial slot (-1
+ * for a whole row). split = 0 gives the whole-row list, 1 the split-KV plan
+ * (the one bs_attention_workspace_bytes sizes). Writes min(*n_items,
+ * max_items) entries to `items` (caller-owned), the list length to *n_items
+ * and the plan's partial-slot count to *n_parts. BS_ERR_UNSUPPORTED outside
+ * the bf16 kernels' shapes; descriptors are not validated.
+ */
+int bs_attention_work_list(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D, bs_dtype dt, int split,
+                           int32_t* items, int max_items, int* n_items, int* n_parts);
 int bs_dual_cache_block_attention(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int Hq,
                                   int Hkv, int D, bs_dtype dt, float scale, const void* q,
                                   const void* k_new, const void* v_new, void* k_cache,
@@ -338,10 +361,15 @@ int bs_kv_scatter_compact(bs_ctx* ctx, const bs_copy_seg* segs, int nseg, int n_
  * and mask, K2 per layer, K3 on the compact state, then K1^-1 scatter; only
  * the gather/scatter launches are saved. pos_out ([n][L] int32, may be NULL)
  * receives s_i + j for j < B_i and -1 beyond. conf_out as for K3 ([n][L]).
- * Other arguments as for K2 and K3 (n_layers == 0 runs K3 alone); ws is K3's
- * workspace: bs_decode_workspace_bytes(n, L, V, logits_dt) bytes. All checks
- * run before anything is enqueued.
+ * Other arguments as for K2 and K3 (n_layers == 0 runs K3 alone). ws: at
+ * least bs_decode_workspace_bytes(n, L, V, logits_dt) bytes (K3's part); with
+ * bs_step_workspace_bytes(...) bytes the attention also runs its split-KV
+ * plan, its partial slots placed after K3's part rounded up to 256 bytes
+ * (see bs_dual_cache_block_attention). All checks run before anything is
+ * enqueued.
  */
+size_t bs_step_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D, bs_dtype dt, int V,
+                               bs_dtype logits_dt);
 int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int R, int W, int n_layers, int Hq,
                         int Hkv, int D, bs_dtype dt, float scale, int write_back, const void* const* q,
                         const void* const* k_new, const void* const* v_new, void* const* k_cache,
@@ -355,7 +383,8 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
  * bs_mixed_state_step for callers that cannot allocate device memory: code
  * under HIP graph capture, serving loops that must not call hipMalloc, and
  * harnesses that forbid allocation. Same arguments, rules and results as
- * bs_mixed_state_step, without the workspace: the descriptors, the attention
+ * bs_mixed_state_step, without the workspace (so every attention row runs
+ * whole, no split-KV): the descriptors, the attention
  * work list and the decode partials go to the library's static device array
  * (8 MiB per GPU, held until the process ends), whose address the context
  * resolved when it was created; the call itself allocates nothing and calls
@@ -363,7 +392,7 @@ int bs_mixed_state_step(bs_ctx* ctx, const bs_req_desc* reqs, int n, int L, int 
  * four pinned stages that bs_create allocated; a call waits for the device
  * only when all four are still being copied from.
  * Limits (BS_ERR_UNSUPPORTED beyond them, before anything is enqueued):
- * n * 20 bytes (rounded up to 16) plus n * Hkv * ceil(L / 32) * 32 bytes of
+ * n * 20 bytes (rounded up to 16) plus n * Hkv * ceil(L / 32) * 48 bytes of
  * work items (the ceil term only when (Hq / Hkv) * ceil(L / 32) > 8, else 1;
  * no work items for BS_F32 or n_layers == 0) within 512 KiB; bs_decode_workspace_bytes(n, L,
  * V, logits_dt) within 7.5 MiB.

@@ -25,7 +25,7 @@ __all__ = [
     "bs_scatter_active_blocks_n", "bs_mixed_state_step", "bs_mixed_state_step_noalloc", "bs_profile_begin", "bs_profile_end",
     "bs_sched_create", "bs_sched_destroy", "bs_sched_submit", "bs_sched_refill", "bs_sched_complete",
     "bs_sched_counts", "bs_sched_last_error", "Scheduler",
-    "bs_attention_workspace_bytes",
+    "bs_attention_workspace_bytes", "bs_step_workspace_bytes", "bs_attention_work_list",
     "bs_dual_cache_block_attention", "bs_decode_workspace_bytes", "bs_parallel_decode",
     "bs_kv_scatter_compact", "bs_lm_head_workspace_bytes", "bs_lm_head_decode", "bs_lm_head_pack_bytes",
     "bs_lm_head_pack", "bs_dual_cache_refresh",
@@ -101,6 +101,9 @@ _SIGS = {
     "bs_dual_cache_block_attention": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                              _vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "bs_decode_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32]),
+    "bs_step_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32]),
+    "bs_attention_work_list": (_i32, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _i32,
+                                      ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
     "bs_parallel_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _f32, _i32, _i32,
                                   _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "bs_lm_head_workspace_bytes": (_sz, [_i32, _i32, _i32]),
@@ -277,8 +280,26 @@ def bs_dual_cache_block_attention(ctx, reqs, L, Hq, Hkv, D, dt, scale, q, k_new,
         _stream(stream)), ctx)
 
 
+def bs_attention_work_list(reqs, L, Hq, Hkv, D, dt, split):
+    """(items [N][6] int32: request, KV head, row block, t0, t1, partial slot;
+    number of partial slots) of the bf16 attention's work list."""
+    r = _host(reqs, REQ_DTYPE)
+    n_items, n_parts = _i32(0), _i32(0)
+    _check(lib.bs_attention_work_list(_ptr(r), len(r), L, Hq, Hkv, D, dt, int(split), None, 0,
+                                      ctypes.byref(n_items), ctypes.byref(n_parts)))
+    out = np.zeros((n_items.value, 6), np.int32)
+    _check(lib.bs_attention_work_list(_ptr(r), len(r), L, Hq, Hkv, D, dt, int(split), _ptr(out), len(out),
+                                      ctypes.byref(n_items), ctypes.byref(n_parts)))
+    return out, n_parts.value
+
+
 def bs_decode_workspace_bytes(n, L, V, dt) -> int:
     return int(lib.bs_decode_workspace_bytes(n, L, V, dt))
+
+
+def bs_step_workspace_bytes(reqs, L, Hq, Hkv, D, dt, V, logits_dt) -> int:
+    r = _host(reqs, REQ_DTYPE)
+    return int(lib.bs_step_workspace_bytes(_ptr(r), len(r), L, Hq, Hkv, D, dt, V, logits_dt))
 
 
 def bs_parallel_decode(ctx, reqs, L, V, logits_dt, logits, logits_row_stride, tokens, masked, tau, q_min,

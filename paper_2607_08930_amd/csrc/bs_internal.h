@@ -34,6 +34,11 @@ __device__ inline void st16(void* p, v4u v) { *reinterpret_cast<v4u*>(p) = v; }
 // ---------------------------------------------------------------- attention
 // One work item = (request, KV head) with the request's geometry resolved on
 // the host, so a workgroup needs a single scalar load before its first DMA.
+// In the shared-tile (GQA) kernel an item may be one piece of a row: keys
+// [64 t0, min(64 t1, len)), with its un-normalised output, running max and
+// row sum going to partial slot `part` for a merge launch (split-KV); part
+// < 0 marks a whole row (t0 = 0, t1 = ceil(len / 64)) written out directly.
+// The single-wave (MHA) kernel always takes whole rows and ignores the three.
 struct AttnItem {
   int32_t req;   // request index (row of q / k_new / v_new / out)
   int32_t kvh;   // KV head
@@ -43,7 +48,23 @@ struct AttnItem {
   int32_t row;   // dense row of the cache
   int32_t off;   // column of logical position 0
   int32_t rb;    // first 32-row block of the block served by this workgroup
+  int32_t t0;    // first 64-key tile of this piece
+  int32_t t1;    // one past its last tile
+  int32_t part;  // partial slot of a split row, or -1
+  int32_t pad;
 };
+
+// One split row: its pieces wrote partial slots [part0, part0 + nparts).
+struct AttnMerge {
+  int32_t req, kvh, rb, B;
+  int32_t part0, nparts, pad0, pad1;
+};
+
+constexpr int kAttnTile = 64;                   // keys per tile of the shared-tile kernel
+// floats of one wave's partial at head dimension D: O^T in accumulator order
+// (D / 8 groups of 4 per lane, 64 lanes), then the running max (log2 units)
+// and the row sum per lane
+__host__ __device__ constexpr int part_wave_floats(int D) { return D / 8 * 64 * 4 + 2 * 64; }
 
 struct AttnArgs {
   const bs_req_desc* reqs;
@@ -67,6 +88,11 @@ struct AttnArgs {
   uint64_t* mask_words;
   const uint8_t* masked;
   int64_t msk_rs;
+  // split-KV: partial slots (part_wave_floats(D) per wave of a workgroup) and the
+  // rows the merge launch combines from them
+  float* parts;
+  const AttnMerge* merges;
+  int n_merge;
 };
 
 constexpr int kMhaWaves = 4;  // waves (independent items) per workgroup of the single-wave bf16 kernel

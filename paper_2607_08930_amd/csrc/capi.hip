@@ -7,8 +7,10 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <memory>
 #include <mutex>
+#include <queue>
 #include <string>
 #include <vector>
 
@@ -38,7 +40,7 @@ struct Slot {
   size_t cap = 0;
   std::vector<unsigned char> key;
   uint64_t hash = 0;
-  int meta[4] = {0, 0, 0, 0};  // blob layout (offsets, counts) recorded at build time
+  int meta[6] = {0, 0, 0, 0, 0, 0};  // blob layout (offsets, counts) recorded at build time
   hipEvent_t ready = nullptr;  // recorded after the upload
   hipEvent_t done = nullptr;   // recorded after the last launch that read it
   hipStream_t stream = nullptr;
@@ -152,7 +154,7 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 // Blob = descriptors followed by an optional work list, 16-byte aligned parts.
 struct Blob {
   std::vector<unsigned char> bytes;
-  int meta[4] = {0, 0, 0, 0};
+  int meta[6] = {0, 0, 0, 0, 0, 0};
   size_t add(const void* p, size_t n) {
     size_t off = (bytes.size() + 15) & ~size_t(15);
     bytes.resize(off + n);
@@ -345,7 +347,9 @@ void attention_items_into(AttnItem* items, AttnItem* tmp, const bs_req_desc* req
   for (int i = 0; i < n; ++i) {
     const Geo gq = geo_of(reqs[i], L);
     for (int h = 0; h < Hkv; ++h)
-      for (int rb = 0; rb < split; ++rb) items[N++] = AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, rb};
+      for (int rb = 0; rb < split; ++rb)
+        items[N++] = AttnItem{i, h, gq.len, gq.s, gq.B, reqs[i].row, reqs[i].off, rb, 0,
+                              (gq.len + kAttnTile - 1) / kAttnTile, -1, 0};
   }
   // longest first; equal lengths keep the (request, head, row block) order
   std::sort(items, items + N, [](const AttnItem& x, const AttnItem& y) {
@@ -362,26 +366,162 @@ void attention_items_into(AttnItem* items, AttnItem* tmp, const bs_req_desc* req
   }
 }
 
-// Descriptors, then (bf16) the work items above.
-void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, bs_dtype dt) {
+// ---- split-KV plan (shared-tile kernel)
+// The shared-tile kernel runs one workgroup per CU (its ring fills the LDS),
+// so a launch of whole rows lasts at least as long as its longest row, while
+// CUs that drew short rows sit idle: the straggler effect of a heterogeneous
+// batch. The plan can cut rows into pieces of 64-key tiles; each piece writes
+// a partial and a merge launch combines a row's pieces. Its estimate of a
+// launch, in tiles of one workgroup's loop, is the larger of
+//  * the list schedule: workgroups longest first on the least-loaded of
+//    kPlanCUs CUs (what the dispatcher does with a list sorted that way),
+//    each costing kPieceOverhead + its tiles, and
+//  * the machine-wide bound: all workgroups' cost over kPlanCUs, times
+//    kFullLoad (a tile takes that much longer when every CU runs the loop
+//    than when few do; measured on the Dream-7B layer: 2.07 against 1.64 us),
+// plus, when anything is cut, the merge launch. Targets T just above the
+// balanced load are tried: a row longer than T - kPieceOverhead tiles is cut
+// into pieces of that many tiles plus the rest. The lowest estimate wins;
+// with none below the whole rows' estimate nothing is cut. So a batch that
+// fills the GPU with rows of similar length runs whole, and a few long rows
+// beside short ones are spread over the idle CUs.
+constexpr int kPlanCUs = 256;
+constexpr double kPieceOverhead = 2.0;
+constexpr double kFullLoad = 1.3;
+constexpr double kMergeFixed = 3.0;        // the merge launch, in tiles
+constexpr double kMergePerPart = 0.02;     // per partial read back
+
+bool shared_tile_path(int L, int Hq, int Hkv) { return !(Hq == Hkv && L <= 32); }
+
+int waves_per_item(int L, int Hq, int Hkv) {
+  const int G = Hq / Hkv, RB = (L + 31) / 32;
+  return G * (G * RB > 8 ? 1 : RB);
+}
+
+// Estimated launch time (tiles) of workgroups of `tiles` tiles each (sorts `tiles`).
+double launch_estimate(std::vector<int>& tiles) {
+  std::sort(tiles.begin(), tiles.end(), std::greater<int>());
+  std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
+  for (int i = 0; i < kPlanCUs; ++i) cu.push(0.0);
+  double end = 0.0, total = 0.0;
+  for (int t : tiles) {
+    const double x = cu.top() + kPieceOverhead + t;
+    cu.pop();
+    cu.push(x);
+    end = std::max(end, x);
+    total += kPieceOverhead + t;
+  }
+  return std::max(end, kFullLoad * total / kPlanCUs);
+}
+
+// Largest piece (tiles) of the best plan for rows of nt[i] tiles, or 0 for no cut.
+int split_cap(const std::vector<int>& nt) {
+  if (nt.empty()) return 0;
+  double total = 0.0;
+  for (int t : nt) total += t + kPieceOverhead;
+  std::vector<int> w(nt);
+  const double whole = launch_estimate(w);
+  const int lb = (int)std::ceil(total / kPlanCUs);
+  if (whole <= kFullLoad * lb + kMergeFixed) return 0;    // no plan can gain
+  double best = whole;
+  int best_cap = 0;
+  for (int T = lb; T <= lb + 5; ++T) {
+    const int cap = T - (int)kPieceOverhead;
+    if (cap < 2) continue;
+    w.clear();
+    int parts = 0;
+    for (int t : nt) {
+      if (t <= cap) {
+        w.push_back(t);
+        continue;
+      }
+      for (int r = t; r > 0; r -= cap) w.push_back(std::min(r, cap));
+      parts += (t + cap - 1) / cap;
+    }
+    const double est = launch_estimate(w) + kMergeFixed + kMergePerPart * parts;
+    if (est < best) {
+      best = est;
+      best_cap = cap;
+    }
+  }
+  return best_cap;
+}
+
+// Cuts the whole rows `items` (as attention_items_into leaves them) into
+// pieces of at most `cap` tiles, sorted longest first; a row's pieces take
+// consecutive partial slots, and `merges` lists the rows that were cut.
+// Returns the number of partial slots.
+int split_items(const std::vector<AttnItem>& items, int cap, std::vector<AttnItem>& pieces,
+                std::vector<AttnMerge>& merges) {
+  int parts = 0;
+  pieces.clear();
+  merges.clear();
+  for (const AttnItem& it : items) {
+    const int nt = it.t1 - it.t0;
+    if (cap <= 0 || nt <= cap) {
+      pieces.push_back(it);
+      continue;
+    }
+    const int np = (nt + cap - 1) / cap;
+    merges.push_back(AttnMerge{it.req, it.kvh, it.rb, it.B, parts, np, 0, 0});
+    for (int k = 0; k < np; ++k) {
+      AttnItem p = it;
+      p.t0 = k * cap;
+      p.t1 = std::min(nt, (k + 1) * cap);
+      p.part = parts + k;
+      pieces.push_back(p);
+    }
+    parts += np;
+  }
+  std::stable_sort(pieces.begin(), pieces.end(), [](const AttnItem& x, const AttnItem& y) {
+    return x.t1 - x.t0 > y.t1 - y.t0;
+  });
+  return parts;
+}
+
+// Partial-slot bytes of a plan with `parts` slots.
+size_t part_bytes(int parts, int L, int Hq, int Hkv, int D) {
+  return (size_t)parts * waves_per_item(L, Hq, Hkv) * part_wave_floats(D) * sizeof(float);
+}
+
+// Descriptors, then (bf16) the work items above, then (split) the merge list;
+// meta = {descriptors, items, item count, merges, merge count, partial slots}.
+void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, bs_dtype dt, bool split) {
   blob.meta[0] = (int)blob.add(reqs, sizeof(bs_req_desc) * n);
   if (dt == BS_BF16) {
     const size_t N = attention_item_count(n, L, Hq, Hkv, dt);
     std::vector<AttnItem> items(N), tmp(N);
     attention_items_into(items.data(), tmp.data(), reqs, n, L, Hq, Hkv);
-    blob.meta[1] = (int)blob.add(items.data(), sizeof(AttnItem) * N);
-    blob.meta[2] = (int)N;
+    int cap = 0;
+    if (split && shared_tile_path(L, Hq, Hkv)) {
+      std::vector<int> nt(N);
+      for (size_t i = 0; i < N; ++i) nt[i] = items[i].t1 - items[i].t0;
+      cap = split_cap(nt);
+    }
+    std::vector<AttnItem> pieces;
+    std::vector<AttnMerge> merges;
+    const int parts = cap > 0 ? split_items(items, cap, pieces, merges) : 0;
+    const std::vector<AttnItem>& list = cap > 0 ? pieces : items;
+    blob.meta[1] = (int)blob.add(list.data(), sizeof(AttnItem) * list.size());
+    blob.meta[2] = (int)list.size();
+    blob.meta[3] = (int)blob.add(merges.data(), sizeof(AttnMerge) * merges.size());
+    blob.meta[4] = (int)merges.size();
+    blob.meta[5] = parts;
   }
 }
 
-// Launch arguments over a device blob at `dblob` laid out as `meta` says.
+// Launch arguments over a device blob at `dblob` laid out as `meta` says;
+// `parts` holds the plan's partial slots (unused when it has none).
 AttnArgs attention_args(const void* dblob, const int* meta, int L, int Hq, int Hkv, int D, int R, int W, float scale,
-                        int write_back) {
+                        int write_back, void* parts) {
   const char* base = static_cast<const char*>(dblob);
   AttnArgs a{};
   a.reqs = reinterpret_cast<const bs_req_desc*>(base + meta[0]);
   a.items = reinterpret_cast<const AttnItem*>(base + meta[1]);
   a.n_items = meta[2];
+  a.merges = reinterpret_cast<const AttnMerge*>(base + meta[3]);
+  a.n_merge = meta[4];
+  a.parts = static_cast<float*>(parts);
   a.L = L; a.Hq = Hq; a.Hkv = Hkv; a.D = D; a.G = Hq / Hkv; a.RB = (L + 31) / 32; a.R = R; a.W = W;
   a.RBW = a.G * a.RB > 8 ? 1 : a.RB;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf((float)D);
@@ -435,6 +575,10 @@ size_t decode_ws_bytes(int n, int L, int V, bs_dtype dt) {
   if (n <= 0 || L <= 0 || V <= 0 || dtype_bytes(dt) == 0) return 0;
   return dec_workspace_bytes(n, L, dec_parts(V, dtype_bytes(dt)));
 }
+
+// The fused step's workspace: the decode's, rounded up to 256 bytes, then the
+// attention's partial slots (split-KV) when the caller provides room for them.
+size_t step_decode_bytes(int n, int L, int V, bs_dtype dt) { return (decode_ws_bytes(n, L, V, dt) + 255) & ~size_t(255); }
 
 // skip_ws: the caller checks (or provides) the workspace itself
 int check_decode(bs_ctx* c, int n, int L, int V, bs_dtype logits_dt, int64_t logits_row_stride, float tau,
@@ -728,8 +872,52 @@ int bs_scatter_active_blocks_n(bs_ctx* c, const bs_req_desc* reqs, int n, int L,
 // ------------------------------------------------------------------ K2
 size_t bs_attention_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
                                     bs_dtype dt) {
-  (void)reqs; (void)n; (void)L; (void)Hq; (void)Hkv; (void)D; (void)dt;
-  return 0;
+  if (!reqs || n <= 0 || dt != BS_BF16 || L < 1 || L > 64 || Hkv < 1 || Hq < Hkv || Hq % Hkv || (D != 64 && D != 128) ||
+      !shared_tile_path(L, Hq, Hkv))
+    return 0;
+  const size_t N = attention_item_count(n, L, Hq, Hkv, dt);
+  std::vector<AttnItem> items(N), tmp(N);
+  attention_items_into(items.data(), tmp.data(), reqs, n, L, Hq, Hkv);
+  std::vector<int> nt(N);
+  for (size_t i = 0; i < N; ++i) nt[i] = std::max(items[i].t1 - items[i].t0, 0);
+  const int cap = split_cap(nt);
+  int parts = 0;
+  if (cap > 0)
+    for (int t : nt)
+      if (t > cap) parts += (t + cap - 1) / cap;
+  return part_bytes(parts, L, Hq, Hkv, D);
+}
+
+int bs_attention_work_list(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D, bs_dtype dt, int split,
+                           int32_t* items, int max_items, int* n_items, int* n_parts) {
+  if (!n_items || !n_parts || (max_items > 0 && !items) || n < 0 || (n > 0 && !reqs))
+    return fail(nullptr, BS_ERR_INVALID_ARG, "bad work-list arguments");
+  if (dt != BS_BF16 || L < 1 || L > 64 || Hkv < 1 || Hq < Hkv || Hq % Hkv || (D != 64 && D != 128))
+    return fail(nullptr, BS_ERR_UNSUPPORTED, "work lists exist for the bf16 kernels only");
+  Blob blob;
+  attention_blob(blob, reqs, n, L, Hq, Hkv, dt, split != 0);
+  const int N = blob.meta[2];
+  *n_items = N;
+  *n_parts = blob.meta[5];
+  const AttnItem* it = reinterpret_cast<const AttnItem*>(blob.bytes.data() + blob.meta[1]);
+  for (int i = 0; i < std::min(N, max_items); ++i) {
+    const int32_t v[6] = {it[i].req, it[i].kvh, it[i].rb, it[i].t0, it[i].t1, it[i].part};
+    std::memcpy(items + 6 * (size_t)i, v, sizeof v);
+  }
+  return BS_OK;
+}
+
+// The attention blob of a call: split (split-KV) when `room` bytes of partial
+// slots hold the plan's, else every row whole.
+int attention_upload(bs_ctx* c, hipStream_t s, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
+                     bs_dtype dt, size_t room, Slot** out) {
+  for (int split = room > 0 ? 1 : 0; split >= 0; --split) {
+    int st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt, split}, reqs, sizeof(bs_req_desc) * n),
+                    [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt, split != 0); }, out);
+    if (st) return st;
+    if (part_bytes((*out)->meta[5], L, Hq, Hkv, D) <= room) return BS_OK;
+  }
+  return BS_OK;   // not reached: the whole-row blob has no partial slots
 }
 
 int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int Hq,
@@ -742,8 +930,6 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   if (st) return st;
   st = check_attention(c, n, L, Hq, Hkv, D, dt);
   if (st) return st;
-  const size_t need = bs_attention_workspace_bytes(reqs, n, L, Hq, Hkv, D, dt);
-  if (ws_bytes < need || (need && !ws)) return fail(c, BS_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   if (n == 0) return BS_OK;
   st = check_attention_tensors(c, q, k_new, v_new, k_cache, v_cache, out, -1);
   if (st) return st;
@@ -751,18 +937,21 @@ int bs_dual_cache_block_attention(bs_ctx* c, const bs_req_desc* reqs, int n, int
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
-              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
+  st = attention_upload(c, s, reqs, n, L, Hq, Hkv, D, dt, ws ? ws_bytes : 0, &sl);
   if (st) return st;
-  AttnArgs a = attention_args(sl->d, sl->meta, L, Hq, Hkv, D, R, W, scale, write_back);
+  AttnArgs a = attention_args(sl->d, sl->meta, L, Hq, Hkv, D, R, W, scale, write_back, ws);
   a.q = q; a.k_new = k_new; a.v_new = v_new; a.k_cache = k_cache; a.v_cache = v_cache; a.out = out;
-  (void)ws;
   hipError_t e = dt == BS_F32 ? launch_attn_f32(a, n, s) : launch_attn_bf16(a, s);
   return finish(c, sl, s, e, "attention launch");
 }
 
 // ------------------------------------------------------------------ K3
 size_t bs_decode_workspace_bytes(int n, int L, int V, bs_dtype dt) { return decode_ws_bytes(n, L, V, dt); }
+
+size_t bs_step_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D, bs_dtype dt, int V,
+                               bs_dtype logits_dt) {
+  return step_decode_bytes(n, L, V, logits_dt) + bs_attention_workspace_bytes(reqs, n, L, Hq, Hkv, D, dt);
+}
 
 int bs_parallel_decode(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int V,
                        bs_dtype logits_dt, const void* logits, int64_t logits_row_stride,
@@ -990,9 +1179,9 @@ static hipError_t step_launch(bs_ctx* c, const void* dblob, const int* meta, int
                               int64_t logits_row_stride, int32_t* tokens, int64_t tokens_row_stride, uint8_t* masked,
                               int64_t masked_row_stride, float tau, int32_t q_min, int32_t eos_id,
                               int32_t* n_unmasked, uint8_t* done, uint8_t* eos_seen, float* conf_out,
-                              int32_t* pos_out, void* ws, hipStream_t s) {
+                              int32_t* pos_out, void* ws, void* part_slots, hipStream_t s) {
   hipError_t e = prof_mark(c, 0, s);
-  AttnArgs a = attention_args(dblob, meta, L, Hq, Hkv, D, R, W, scale, write_back);
+  AttnArgs a = attention_args(dblob, meta, L, Hq, Hkv, D, R, W, scale, write_back, part_slots);
   // the bf16 attention of the first layer also leaves each request's block
   // mask word behind the decode partials, for the row reductions below
   const int parts = dec_parts(V, dtype_bytes(logits_dt));
@@ -1037,14 +1226,16 @@ int bs_mixed_state_step(bs_ctx* c, const bs_req_desc* reqs, int n, int L, int R,
   DeviceGuard dg(c->device);
   if (!dg.ok) return fail(c, BS_ERR_HIP, "hipSetDevice(%d) failed", c->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // the workspace past the decode's (rounded to 256 bytes) holds the
+  // attention's partial slots when it is large enough for the split plan
+  const size_t dws = step_decode_bytes(n, L, V, logits_dt);
   Slot* sl = nullptr;
-  st = upload(c, s, Key('A', {n, L, Hq, Hkv, (int64_t)dt}, reqs, sizeof(bs_req_desc) * n),
-              [&](Blob& blob) { attention_blob(blob, reqs, n, L, Hq, Hkv, dt); }, &sl);
+  st = attention_upload(c, s, reqs, n, L, Hq, Hkv, D, dt, n_layers > 0 && ws_bytes > dws ? ws_bytes - dws : 0, &sl);
   if (st) return st;
   hipError_t e = step_launch(c, sl->d, sl->meta, n, L, R, W, n_layers, Hq, Hkv, D, dt, scale, write_back, q, k_new,
                              v_new, k_cache, v_cache, out, V, logits_dt, logits, logits_row_stride, tokens,
                              tokens_row_stride, masked, masked_row_stride, tau, q_min, eos_id, n_unmasked, done,
-                             eos_seen, conf_out, pos_out, ws, s);
+                             eos_seen, conf_out, pos_out, ws, static_cast<unsigned char*>(ws) + dws, s);
   return finish(c, sl, s, e, "step launch");
 }
 
@@ -1102,7 +1293,7 @@ int bs_mixed_state_step_noalloc(bs_ctx* c, const bs_req_desc* reqs, int n, int L
   unsigned char* h = static_cast<unsigned char*>(sp.stage[k]);
   std::memcpy(h, reqs, sizeof(bs_req_desc) * n);
   if (n_items) attention_items_into(reinterpret_cast<AttnItem*>(h + items_off), sp.tmp.get(), reqs, n, L, Hq, Hkv);
-  const int meta[4] = {0, (int)items_off, (int)n_items, 0};
+  const int meta[6] = {0, (int)items_off, (int)n_items, 0, 0, 0};   // whole rows: no merge list
   hipError_t e = hipMemcpyAsync(dscratch, h, blob_bytes, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync(scratch)");
   e = hipEventRecord(sp.copied[k], s);
@@ -1110,7 +1301,7 @@ int bs_mixed_state_step_noalloc(bs_ctx* c, const bs_req_desc* reqs, int n, int L
   e = step_launch(c, dscratch, meta, n, L, R, W, n_layers, Hq, Hkv, D, dt, scale, write_back, q, k_new, v_new,
                   k_cache, v_cache, out, V, logits_dt, logits, logits_row_stride, tokens, tokens_row_stride, masked,
                   masked_row_stride, tau, q_min, eos_id, n_unmasked, done, eos_seen, conf_out, pos_out,
-                  dscratch + kStaticBlobBytes, s);
+                  dscratch + kStaticBlobBytes, nullptr, s);
   if (e != hipSuccess) return hip_fail(c, e, "no-alloc step launch");
   return BS_OK;
 }

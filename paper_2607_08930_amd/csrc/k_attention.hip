@@ -33,6 +33,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ inline float wave_max(float v) {
 #pragma unroll
@@ -317,13 +318,16 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
       }
     }
   };
-  const int ntiles = (len + KT - 1) / KT;
+  // tiles of this item: the whole row, or (shared-tile kernel) one piece of
+  // it, keys [tb0, tb0 + ntiles * KT) clamped to the row
+  const int tb0 = SHARED ? it.t0 * KT : 0;
+  const int ntiles = SHARED ? it.t1 - it.t0 : (len + KT - 1) / KT;
   // The request's block mask word, in the fused step (one item per request:
   // KV head 0, first row block, its first wave): lane j reads mask cell j of
   // the block, by inline assembly so the compiler adds no wait of its own;
   // issued before the DMA, so every later wait of this wave covers it, and
   // consumed after the last one.
-  const bool word_owner = a.mask_words != nullptr && it.kvh == 0 && it.rb == 0 && wg == 0;
+  const bool word_owner = a.mask_words != nullptr && it.kvh == 0 && it.rb == 0 && it.t0 == 0 && wg == 0;
   uint32_t mcell = 0;
   if (word_owner) {
     const uint8_t* mp = a.masked + it.row * a.msk_rs + it.off + it.s + (lane < it.B ? lane : 0);
@@ -334,7 +338,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
   if (issuer) {
 #pragma unroll
     for (int st = 0; st < NS - 1; ++st)
-      if (st < ntiles) issue(st, st * KT);
+      if (st < ntiles) issue(st, tb0 + st * KT);
   }
 
   // queries of this lane's column as MFMA B operands: feature d = 16 kk + 8 g + e
@@ -438,7 +442,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
 
     auto body = [&](auto first_tag, int tile) {
       constexpr bool FIRST = decltype(first_tag)::value;
-      const int tb = tile * KT;
+      const int tb = tb0 + tile * KT;
       const uint16_t* vprev = ring + ((tile + NS - 1) % NS) * STAGE + TILE;
       mask_ragged(tb);
       // ---- block 1
@@ -506,7 +510,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
         if (issuer) wait_stages(min(ntiles - 1, tile + NS - 2) - tile - 1);
         __syncthreads();
         const int nxt = tile + NS - 1;
-        if (issuer && nxt < ntiles) issue(nxt % NS, nxt * KT);
+        if (issuer && nxt < ntiles) issue(nxt % NS, tb0 + nxt * KT);
       }
       // ---- block 2 (on the last tile the scores read a resident slot and
       // are discarded)
@@ -662,42 +666,60 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     }
   }
   const float lt = xhalf_sum(lsum);
-  // Output: lane (g, n) holds O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4]
-  // [query n]. The wave's 32 x D tile is staged row-major in LDS (rows padded
-  // by 16 bytes against bank conflicts) and stored as whole rows, 16 bytes per
-  // lane, instead of 8-byte pieces scattered over 32 rows. The stores are
-  // non-temporal: the output is not read again by the step, and whole lines
-  // written around the L2 leave no dirty lines for the kernels that follow
-  // to evict (measured: the Dream-7B step's decode rows 61.5 -> 57.7 us).
-  if constexpr (SHARED) __syncthreads();          // every wave is done with the ring
-  constexpr int SROW = D + 8;                     // staged row stride (elements)
-  uint16_t* stg = ring + (SHARED ? wg * 32 * SROW : 0);
-  {
-    const float inv = (j < it.B) ? 1.0f / lt : 0.0f;
-    typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+  bool whole = true;
+  if constexpr (SHARED) whole = it.part < 0;
+  if (!whole) {
+    // One piece of a split row: the un-normalised O^T (accumulator order,
+    // whole 16-byte groups per lane), the running max in log2 units and the
+    // row sum go to the piece's partial slot for the merge launch.
+    constexpr int OFL = NDT * 16 * 64;
+    float* pw = a.parts + ((int64_t)it.part * GW + wg) * part_wave_floats(D);
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const __bf16 b0 = (__bf16)(o[dt][4 * rq + 0] * inv);
-        const __bf16 b1 = (__bf16)(o[dt][4 * rq + 1] * inv);
-        const __bf16 b2 = (__bf16)(o[dt][4 * rq + 2] * inv);
-        const __bf16 b3 = (__bf16)(o[dt][4 * rq + 3] * inv);
-        const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
-        const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) | ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
-        *reinterpret_cast<v2u*>(stg + n * SROW + dt * 32 + 8 * rq + 4 * g) = v2u{w0, w1};
-      }
-  }
-  {
-    constexpr int RPW = 64 / NCH;                 // rows per wave instruction
-    const int jb = (it.rb + wg % a.RBW) * 32;     // first block row of this wave
+      for (int rq = 0; rq < 4; ++rq)
+        __builtin_nontemporal_store(f32x4_t{o[dt][4 * rq], o[dt][4 * rq + 1], o[dt][4 * rq + 2], o[dt][4 * rq + 3]},
+                                    reinterpret_cast<f32x4_t*>(pw + ((dt * 4 + rq) * 64 + lane) * 4));
+    __builtin_nontemporal_store(mrun, pw + OFL + lane);
+    __builtin_nontemporal_store(lt, pw + OFL + 64 + lane);
+  } else {
+    // Output: lane (g, n) holds O^T[feature dt*32 + 8 (rr / 4) + 4 g + rr % 4]
+    // [query n]. The wave's 32 x D tile is staged row-major in LDS (rows padded
+    // by 16 bytes against bank conflicts) and stored as whole rows, 16 bytes per
+    // lane, instead of 8-byte pieces scattered over 32 rows. The stores are
+    // non-temporal: the output is not read again by the step, and whole lines
+    // written around the L2 leave no dirty lines for the kernels that follow
+    // to evict (measured: the Dream-7B step's decode rows 61.5 -> 57.7 us).
+    if constexpr (SHARED) __syncthreads();          // every wave is done with the ring
+    constexpr int SROW = D + 8;                     // staged row stride (elements)
+    uint16_t* stg = ring + (SHARED ? wg * 32 * SROW : 0);
+    {
+      const float inv = (j < it.B) ? 1.0f / lt : 0.0f;
+      typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 #pragma unroll
-    for (int k = 0; k < 32 / RPW; ++k) {
-      const int row = k * RPW + lane / NCH, c = lane % NCH;
-      const v4u v = *reinterpret_cast<const v4u*>(stg + row * SROW + c * 8);
-      if (jb + row < a.L) {
-        uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)it.req * a.L + jb + row) * a.Hq + h) * D;
-        __builtin_nontemporal_store(v, reinterpret_cast<v4u*>(op + c * 8));
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const __bf16 b0 = (__bf16)(o[dt][4 * rq + 0] * inv);
+          const __bf16 b1 = (__bf16)(o[dt][4 * rq + 1] * inv);
+          const __bf16 b2 = (__bf16)(o[dt][4 * rq + 2] * inv);
+          const __bf16 b3 = (__bf16)(o[dt][4 * rq + 3] * inv);
+          const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
+          const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) | ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
+          *reinterpret_cast<v2u*>(stg + n * SROW + dt * 32 + 8 * rq + 4 * g) = v2u{w0, w1};
+        }
+    }
+    {
+      constexpr int RPW = 64 / NCH;                 // rows per wave instruction
+      const int jb = (it.rb + wg % a.RBW) * 32;     // first block row of this wave
+#pragma unroll
+      for (int k = 0; k < 32 / RPW; ++k) {
+        const int row = k * RPW + lane / NCH, c = lane % NCH;
+        const v4u v = *reinterpret_cast<const v4u*>(stg + row * SROW + c * 8);
+        if (jb + row < a.L) {
+          uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)it.req * a.L + jb + row) * a.Hq + h) * D;
+          __builtin_nontemporal_store(v, reinterpret_cast<v4u*>(op + c * 8));
+        }
       }
     }
   }
@@ -734,6 +756,73 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
   attn_item<D, 64, NS, true, NI, 0>(a, a.items[blockIdx.x], lds, blockDim.x >> 6, w, threadIdx.x & 63);
 }
 
+// Split-KV merge: one wave per (split row, wave slot wg of its pieces'
+// workgroups), serving the same query head (kvh * G + wg / RBW) and 32 block
+// rows (row block rb + wg % RBW) as those waves. Lane (g, n) folds the
+// pieces' partials of its query column in order, keeping a running max m:
+// the sums so far are scaled by 2^(m_old - m) and piece p's by 2^(m_p - m)
+// (the log-sum-exp merge of softmax pieces); the quotient is written like the
+// attention's own output (bf16; rows B .. L - 1 as zeros). The next piece's
+// loads are issued before the current one is folded.
+template <int D>
+__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
+  constexpr int NG = D / 8;                       // groups of 4 floats per lane
+  constexpr int OFL = NG * 64 * 4;
+  const int GW = a.G * a.RBW;
+  const int idx = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (idx >= a.n_merge * GW) return;
+  const int wg = idx % GW;
+  const AttnMerge mg = a.merges[idx / GW];
+  const int g = lane >> 5, n = lane & 31;
+  const int h = mg.kvh * a.G + wg / a.RBW;
+  const int j = (mg.rb + wg % a.RBW) * 32 + n;
+  const int64_t pstride = (int64_t)GW * part_wave_floats(D);
+  const float* pw = a.parts + ((int64_t)mg.part0 * GW + wg) * part_wave_floats(D);
+  f32x4_t cur[NG], nxt[NG], acc[NG];
+  float cm = pw[OFL + lane], cl = pw[OFL + 64 + lane], nm = 0.0f, nl = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NG; ++k) {
+    cur[k] = *reinterpret_cast<const f32x4_t*>(pw + (k * 64 + lane) * 4);
+    acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  float m = -__builtin_inff(), l = 0.0f;
+  for (int p = 0; p < mg.nparts; ++p) {
+    if (p + 1 < mg.nparts) {
+      const float* pn = pw + (p + 1) * pstride;
+      nm = pn[OFL + lane];
+      nl = pn[OFL + 64 + lane];
+#pragma unroll
+      for (int k = 0; k < NG; ++k) nxt[k] = *reinterpret_cast<const f32x4_t*>(pn + (k * 64 + lane) * 4);
+    }
+    const float mn = fmaxf(m, cm);
+    const float sa = __builtin_amdgcn_exp2f(m - mn), sb = __builtin_amdgcn_exp2f(cm - mn);
+    l = fmaf(l, sa, cl * sb);
+#pragma unroll
+    for (int k = 0; k < NG; ++k) acc[k] = acc[k] * sa + cur[k] * sb;
+    m = mn;
+    cm = nm;
+    cl = nl;
+#pragma unroll
+    for (int k = 0; k < NG; ++k) cur[k] = nxt[k];
+  }
+  if (j >= a.L) return;
+  const float inv = j < mg.B ? 1.0f / l : 0.0f;
+  uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)mg.req * a.L + j) * a.Hq + h) * D + 4 * g;
+  typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int k = 0; k < NG; ++k) {
+    // group k = 4 dt + rq holds features 32 dt + 8 rq + 4 g .. + 3
+    const int d = 32 * (k >> 2) + 8 * (k & 3);
+    uint32_t w2[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const __bf16 lo = (__bf16)(acc[k][2 * e] * inv), hi = (__bf16)(acc[k][2 * e + 1] * inv);
+      w2[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    __builtin_nontemporal_store(v2u{w2[0], w2[1]}, reinterpret_cast<v2u*>(op + d));
+  }
+}
+
 template <int D>
 hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   if (GW == 1) {
@@ -744,6 +833,8 @@ hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   } else {
     hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 4>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   }
+  if (GW > 1 && a.n_merge > 0)
+    hipLaunchKernelGGL((k_attn_merge<D>), dim3((a.n_merge * GW + 3) / 4), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -42,6 +42,7 @@ import numpy as np
 import torch
 
 from . import (SCHED_BUDGET, Context, Scheduler, bs_decode_workspace_bytes, bs_dual_cache_refresh,
+               bs_step_workspace_bytes,
                bs_kv_scatter_compact, bs_mixed_state_step)
 from .step import dt_code, torch_dtype
 
@@ -160,6 +161,11 @@ class Server:
             res.admitted.append(plan["admitted"].tolist())
             res.active_counts.append(n)
             eos_any = np.zeros(n, np.uint8)
+            # the cycle's descriptors are fixed: size the workspace for their
+            # split-KV plan once
+            need = bs_step_workspace_bytes(descs, cfg.L, cfg.Hq, cfg.Hkv, cfg.D, dt, cfg.V, dt)
+            if need > self.ws.numel():
+                self.ws = torch.empty(need, dtype=torch.uint8, device=self.ws.device)
             for step in range(cfg.L):
                 layers, logits = self.provider.step(ids, descs, res.cycles, step)
                 lay = [(q, kn, vn, self.k_box[l], self.v_box[l], self.out[l][:n])

@@ -18,6 +18,7 @@ import numpy as np
 import torch
 
 from . import (BS_BF16, BS_F32, Context, bs_decode_workspace_bytes, bs_dual_cache_block_attention,
+               bs_step_workspace_bytes,
                bs_gather_active_blocks_n, bs_kv_scatter_compact, bs_mixed_state_step, bs_parallel_decode,
                bs_scatter_active_blocks_n)
 
@@ -81,7 +82,8 @@ class StepState:
     done: torch.Tensor = None
     eos_seen: torch.Tensor = None
     conf: torch.Tensor = None
-    dec_ws: torch.Tensor = None
+    dec_ws: torch.Tensor = None      # the step's workspace: the decode's, then the attention's partials
+    ws_key: bytes = None             # descriptors dec_ws was last sized for
     flags_host: torch.Tensor = None
     extra: dict = field(default_factory=dict)
 
@@ -99,24 +101,39 @@ class StepState:
         self.dec_ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
         return self
 
+    def workspace_for(self, reqs: np.ndarray) -> torch.Tensor:
+        """The step workspace, grown to what the descriptors' split-KV plan
+        needs (queried again only when the descriptors change)."""
+        key = reqs.tobytes()
+        if key != self.ws_key:
+            dt = dt_code(self.dtype)
+            need = bs_step_workspace_bytes(reqs, self.L, self.Hq, self.Hkv, self.D, dt, self.V, dt)
+            if need > self.dec_ws.numel():
+                self.dec_ws = torch.empty(need, dtype=torch.uint8, device=self.dec_ws.device)
+            self.ws_key = key
+        return self.dec_ws
+
 
 def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want_conf=False,
-             layers=None, fused=True) -> None:
+             layers=None, fused=True, split=True) -> None:
     """Enqueue one step for the requests ``reqs`` (REQ_DTYPE, n <= n_max).
 
     fused: one library call; the compact tok_c/msk_c are then not written.
-    pos is written either way."""
+    pos is written either way. split: give the attention room for its
+    split-KV plan (else only the decode's workspace: every row whole)."""
     L, R, W = st.L, st.R, st.W
     dt = dt_code(st.dtype)
     lays = st.layers if layers is None else layers
     conf = st.conf if want_conf else None
+    ws = st.workspace_for(reqs)
+    ws_bytes = ws.numel() if split else bs_decode_workspace_bytes(len(reqs), L, st.V, dt)
     if fused:
         bs_mixed_state_step(ctx, reqs, L, R, W,
                             [(x.q, x.k_new, x.v_new, x.k_cache, x.v_cache, x.out) for x in lays],
                             st.Hq, st.Hkv, st.D, dt, st.scale, st.write_back, st.V, dt, st.logits,
                             st.logits.stride(1), st.tokens, st.tokens.stride(0), st.mask, st.mask.stride(0),
                             st.tau, st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, conf, st.pos,
-                            st.dec_ws, st.dec_ws.numel(), stream=stream)
+                            ws, ws_bytes, stream=stream)
         return
     strides = [st.tokens.stride(0) * 4, st.mask.stride(0)]
     bs_gather_active_blocks_n(ctx, reqs, L, R, W, [st.tokens, st.mask], strides, [4, 1], [st.tok_c, st.msk_c],
@@ -124,10 +141,10 @@ def run_step(ctx: Context, st: StepState, reqs: np.ndarray, *, stream=None, want
     for lay in lays:
         bs_dual_cache_block_attention(ctx, reqs, L, st.Hq, st.Hkv, st.D, dt, st.scale, lay.q, lay.k_new,
                                       lay.v_new, lay.k_cache, lay.v_cache, R, W, st.write_back, lay.out,
-                                      None, 0, stream=stream)
+                                      ws if split else None, ws_bytes if split else 0, stream=stream)
     bs_parallel_decode(ctx, reqs, L, st.V, dt, st.logits, st.logits.stride(1), st.tok_c, st.msk_c, st.tau,
-                       st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, conf, st.dec_ws,
-                       st.dec_ws.numel(), stream=stream)
+                       st.q_min, st.eos_id, st.n_unmasked, st.done, st.eos_seen, conf, ws,
+                       ws_bytes, stream=stream)
     bs_scatter_active_blocks_n(ctx, reqs, L, R, W, [st.tok_c, st.msk_c], [4, 1], [st.tokens, st.mask], strides,
                                stream=stream)
 

@@ -35,8 +35,10 @@ def widen_out(x, dtype):
 
 
 def run_attention(ctx, w, layer=0, *, poison=False, write_back=True, reqs=None, q=None, kn=None, vn=None,
-                  kc=None, vc=None, scale=0.0):
-    """Returns (out, k_cache', v_cache', inputs) as host arrays."""
+                  kc=None, vc=None, scale=0.0, split=True):
+    """Returns (out, k_cache', v_cache', inputs) as host arrays. split: pass
+    the workspace the descriptors' split-KV plan asks for (else none, so
+    every row runs whole)."""
     torch, bs, bstep = lazy()
     reqs = w.reqs if reqs is None else reqs
     q = synth.gen_q(w, layer) if q is None else q
@@ -50,8 +52,12 @@ def run_attention(ctx, w, layer=0, *, poison=False, write_back=True, reqs=None, 
     dkn, dvn = bstep.to_device(kn, w.dtype), bstep.to_device(vn, w.dtype)
     dkc, dvc = bstep.to_device(kc, w.dtype), bstep.to_device(vc, w.dtype)
     out = torch.full(dq.shape, float("nan"), dtype=dq.dtype, device="cuda")
-    bs.bs_dual_cache_block_attention(ctx, reqs, w.L, w.Hq, w.Hkv, w.D, bstep.dt_code(w.dtype), scale, dq, dkn,
-                                     dvn, dkc, dvc, w.R, w.W, write_back, out)
+    dt = bstep.dt_code(w.dtype)
+    nws = bs.bs_attention_workspace_bytes(reqs, w.L, w.Hq, w.Hkv, w.D, dt) if split else 0
+    # garbage, not zeros: the partial slots need no initialisation
+    ws = torch.full((nws,), 0xA5, dtype=torch.uint8, device="cuda") if nws else None
+    bs.bs_dual_cache_block_attention(ctx, reqs, w.L, w.Hq, w.Hkv, w.D, dt, scale, dq, dkn,
+                                     dvn, dkc, dvc, w.R, w.W, write_back, out, ws, nws)
     torch.cuda.synchronize()
     return (bstep.to_host(out), bstep.to_host(dkc), bstep.to_host(dvc),
             dict(q=q, k_new=kn, v_new=vn, k_cache=kc, v_cache=vc))

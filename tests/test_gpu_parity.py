@@ -7,7 +7,7 @@ import pytest
 import oracle
 import synth
 from gpu_util import (ATT_TOL, check_attention, check_decode, lazy, run_attention,
-                      run_decode, say)
+                      run_decode, say, widen_out)
 
 pytestmark = pytest.mark.gpu
 
@@ -424,19 +424,86 @@ def test_attention_no_write_back_leaves_cache(ctx):
 
 
 def test_attention_batch_invariance_and_determinism(ctx):
+    # whole rows (no workspace): a request's output is bit-identical alone,
+    # in the batch and in a permuted batch
     w = synth.workload(3)
-    full, _, _, inp = run_attention(ctx, w)
-    again, _, _, _ = run_attention(ctx, w)
+    full, _, _, inp = run_attention(ctx, w, split=False)
+    again, _, _, _ = run_attention(ctx, w, split=False)
     assert np.array_equal(full, again), "run-to-run results differ"
     for i in (0, 17, 63):
         one, _, _, _ = run_attention(ctx, w, reqs=w.reqs[i:i + 1], q=inp["q"][i:i + 1],
                                      kn=inp["k_new"][i:i + 1], vn=inp["v_new"][i:i + 1],
-                                     kc=inp["k_cache"], vc=inp["v_cache"])
+                                     kc=inp["k_cache"], vc=inp["v_cache"], split=False)
         assert np.array_equal(one[0], full[i]), f"request {i} alone differs from in-batch"
     perm = np.random.default_rng(0).permutation(w.n)
     pm, _, _, _ = run_attention(ctx, w, reqs=w.reqs[perm], q=inp["q"][perm], kn=inp["k_new"][perm],
-                                vn=inp["v_new"][perm], kc=inp["k_cache"], vc=inp["v_cache"])
+                                vn=inp["v_new"][perm], kc=inp["k_cache"], vc=inp["v_cache"], split=False)
     assert np.array_equal(pm, full[perm]), "permuted batch differs"
+
+
+def _rows_cut(bs, w):
+    items, parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
+    cut = items[items[:, 5] >= 0]
+    per_row = {}
+    for r in cut:
+        per_row[(r[0], r[1], r[2])] = per_row.get((r[0], r[1], r[2]), 0) + 1
+    return parts, per_row
+
+
+def test_attention_split_kv_matches_whole_rows(ctx):
+    # a Dream-7B batch with one 8000-key row: the plan cuts that row's four
+    # KV heads; the split launch, the whole-row launch and the oracle agree,
+    # the split launch is deterministic, and a request run alone (not cut)
+    # matches its in-batch result within rounding
+    _, bs, _ = lazy()
+    rng = np.random.default_rng(2)
+    n = 24
+    p = rng.integers(128, 1024, n)
+    p[n // 3] = 8000
+    w = synth.custom(32, 28, 4, 128, 10, "bf16", p.tolist(), [512] * n, rng.integers(0, 16, n).tolist(),
+                     kv_sigma=0.1, q_sigma=3.0)
+    parts, per_row = _rows_cut(bs, w)
+    say(f"[split-KV straggler] {len(per_row)} rows cut into {parts} pieces")
+    assert parts > 0 and len(per_row) > 0
+    split, _ = _att(ctx, w, "straggler split-KV", split=True)
+    whole, _ = _att(ctx, w, "straggler whole rows", split=False)
+    again, _, _, inp = run_attention(ctx, w, split=True)
+    assert np.array_equal(split, again), "split-KV run-to-run results differ"
+    d = np.abs(widen_out(split, w.dtype) - widen_out(whole, w.dtype))
+    assert d.max() <= ATT_TOL["bf16"], f"split vs whole rows: {d.max():.3e}"
+    i = n // 3
+    one, _, _, _ = run_attention(ctx, w, reqs=w.reqs[i:i + 1], q=inp["q"][i:i + 1], kn=inp["k_new"][i:i + 1],
+                                 vn=inp["v_new"][i:i + 1], kc=inp["k_cache"], vc=inp["v_cache"])
+    assert np.abs(widen_out(one[0], w.dtype) - widen_out(split[i], w.dtype)).max() <= ATT_TOL["bf16"]
+
+
+def test_attention_split_kv_stragglers(ctx):
+    # one or two rows far longer than the rest of a small batch: the plan cuts
+    # them into many pieces (several partials per merged row), also with two
+    # row blocks per workgroup (L = 64, G = 4, D = 64) and one row block per
+    # workgroup (L = 64, G = 7), and with the fresh block inside a cut piece
+    _, bs, _ = lazy()
+    rng = np.random.default_rng(5)
+    cases = [
+        ("G7 L32 D128", 32, 28, 4, 128, 6000, 40),
+        ("G4 L64 D64", 64, 8, 2, 64, 5000, 30),
+        ("G7 L64 D128", 64, 28, 4, 128, 3000, 12),
+        ("G2 L32 D128", 32, 4, 2, 128, 9000, 60),
+    ]
+    for label, L, Hq, Hkv, D, long_p, n in cases:
+        p = rng.integers(16, 300, n)
+        p[0] = long_p
+        p[n // 2] = long_p // 2
+        g = rng.integers(1, 5, n) * L - rng.integers(0, 2, n) * (L // 4)
+        g = np.maximum(g, 1)
+        K = (g + L - 1) // L
+        k = np.array([rng.integers(0, kk) for kk in K])
+        k[0] = K[0] // 2
+        w = synth.custom(L, Hq, Hkv, D, 10, "bf16", p.tolist(), g.tolist(), k.tolist(), kv_sigma=0.1, q_sigma=3.0)
+        parts, per_row = _rows_cut(bs, w)
+        say(f"[split-KV {label}] {len(per_row)} rows cut into {parts} pieces, at most {max(per_row.values(), default=0)} per row")
+        assert max(per_row.values(), default=0) >= 3, "the straggler rows should be cut into several pieces"
+        _att(ctx, w, f"{label} stragglers")
 
 
 def test_attention_rejects_unsupported(ctx):

@@ -87,7 +87,9 @@ def test_noalloc_step_equals_step_with_workspace(ctx):
         for x in b.layers + a.layers:
             x.out.fill_(float("nan"))
         torch.cuda.synchronize()
-        bstep.run_step(ctx, a, reqs, want_conf=True)
+        # the no-alloc step runs every attention row whole (no room for
+        # split-KV partials), like the step given only the decode's workspace
+        bstep.run_step(ctx, a, reqs, want_conf=True, split=False)
         noalloc_step(ctx, b, reqs)
         torch.cuda.synchronize()
         ga, gb = outputs(a, len(reqs)), outputs(b, len(reqs))
@@ -110,7 +112,7 @@ def test_noalloc_step_rejects_sizes_beyond_the_array(ctx):
                                        bs.BS_BF16, None, 262144, None, 64, None, 64, 0.9, 1, -1, None, None, None,
                                        None, None)
     assert e.value.name == "BS_ERR_UNSUPPORTED"
-    # work items: 2048 requests x 8 KV heads x 32 B = 512 KiB, plus the descriptors
+    # work items: 2048 requests x 8 KV heads x 48 B = 768 KiB, plus the descriptors
     n = 2048
     reqs = np.zeros(n, bs.REQ_DTYPE)
     reqs["g"] = 32

@@ -546,7 +546,8 @@ def kernel_summary(args):
     lines = [f"# Kernel durations: {name}", "", "Commands (repo root as `$R`, one MI355X):", "", "```",
              "cd /tmp && export TMPDIR=/tmp",
              f"rocprofv3 --kernel-trace --stats -d <dir> -o run --output-format csv -- python3 $R/bench.py {cmd}",
-             f"python3 $R/bench.py --kernel-summary <dir> {name} --bench-args='{cmd}'", "```", "",
+             f"python3 $R/bench.py --kernel-summary <dir> {name} --bench-args='{cmd}' --steps {args.steps} "
+             f"--warmup {args.warmup}", "```", "",
              "| kernel | launches | mean us | min us | max us |", "|---|---:|---:|---:|---:|"]
     for k in sorted(per, key=lambda k: -sum(per[k])):
         v = per[k]
@@ -581,6 +582,27 @@ def kernel_summary(args):
         lines += ["", f"Per region (mean us per launch; regions by launch order for --warmup {W} --steps {K}):", "",
                   "| attention kernel | region | steps | attention | decode rows | selection |",
                   "|---|---|---:|---:|---:|---:|"] + region_lines
+    if "--stragglers" in cmd:
+        # launch order of the straggler bench: per batch, W + K whole-row
+        # launches, then W + K split-KV launches each followed by its merge
+        att = [k for k in ks if "k_attn" in k[2] and "merge" not in k[2]]
+        mrg = [k for k in ks if "k_attn_merge" in k[2]]
+        W, K = args.warmup, args.steps
+        lines += ["", f"Per batch and mode (mean over the {K} timed launches after {W} warm-up ones; the split-KV "
+                  "span runs from the attention's start to the merge's end):", "",
+                  "| batch | mode | attention us | merge us | span us |", "|---|---|---:|---:|---:|"]
+        mi = 0
+        for case in range(len(att) // (2 * (W + K))):
+            base = case * 2 * (W + K)
+            whole = att[base + W:base + W + K]
+            lines.append(f"| {case} | whole rows | {np.mean([(b - a) / 1e3 for a, b, _ in whole]):.2f} | - | - |")
+            split = att[base + 2 * W + K:base + 2 * (W + K)]
+            ms = mrg[mi + W:mi + W + K]
+            mi += W + K
+            if len(ms) == len(split):
+                lines.append(f"| {case} | split-KV | {np.mean([(b - a) / 1e3 for a, b, _ in split]):.2f} | "
+                             f"{np.mean([(b - a) / 1e3 for a, b, _ in ms]):.2f} | "
+                             f"{np.mean([(m[1] - a[0]) / 1e3 for a, m in zip(split, ms)]):.2f} |")
     lines.append("")
     fn = os.path.join(ROOT, "profiles", f"{name}_kernel_stats.md")
     open(fn, "w").write("\n".join(lines))
@@ -765,6 +787,77 @@ def lm_head_bench(args):
                                "kind": "oracle",
                                "sample": f"{reps} requests' decoding steps with the output head (fp64), {el:.1f} s"}
     print(json.dumps(res), flush=True)
+
+
+def stragglers_bench(args):
+    """Attention of one layer on straggler batches (synth.straggler: a few rows
+    far longer than the rest of a Dream-7B-shaped batch), whole rows against
+    the split-KV plan. Each launch is bracketed by HIP events on its stream,
+    enqueued behind a 512 MiB read sweep (so the host call overlaps the sweep
+    and the region holds the launch alone, with a cold Infinity Cache).
+    Inputs are drawn on the device (queries and fresh K/V ~ N(0, 1), cache ~
+    N(0, 1/D)). Prints one JSON line."""
+    import torch
+    import synth
+    import paper_2607_08930_amd as bs
+
+    torch.cuda.set_device(0)
+    ctx = bs.Context(0)
+    stream = torch.cuda.current_stream()
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(7)
+
+    def draw(shape, sigma):
+        x = torch.empty(shape, dtype=torch.float32, device="cuda").normal_(0.0, sigma, generator=gen)
+        return x.to(torch.bfloat16)
+
+    results = []
+    for case in (0, 1):
+        w = synth.straggler(case)
+        print(f"[bench] stragglers: {w.name}", file=sys.stderr, flush=True)
+        q = draw((w.n, w.L, w.Hq, w.D), 1.0)
+        kn, vn = draw((w.n, w.L, w.Hkv, w.D), 1.0), draw((w.n, w.L, w.Hkv, w.D), 1.0)
+        kc, vc = draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5), draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5)
+        out = torch.empty_like(q)
+        torch.cuda.synchronize()
+        ab = algorithmic_bytes(w)
+        lens = w.reqs["p"] + w.reqs["g"]
+        entry = {"workload": w.name, "n_requests": int(w.n), "max_len": int(lens.max()), "sum_len": int(lens.sum()),
+                 "algorithmic_bytes": int(ab["attn"])}
+        for split in (False, True):
+            nws = bs.bs_attention_workspace_bytes(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16) if split else 0
+            ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+
+            def call():
+                bs.bs_dual_cache_block_attention(ctx, w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 0.0, q, kn, vn,
+                                                 kc, vc, w.R, w.W, 1, out, ws if nws else None, nws,
+                                                 stream=stream)
+
+            for _ in range(args.warmup):
+                call()
+            ts = []
+            for _ in range(args.steps):
+                flush.sum()
+                e0, e1 = region_events()
+                e0.record(stream)
+                call()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            items, parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, int(split))
+            ms = float(np.median(ts))
+            entry["split_kv" if split else "whole_rows"] = {
+                "ms": round(ms, 5), "workgroups": int(len(items)), "partial_slots": int(parts),
+                "longest_workgroup_tiles": int((items[:, 4] - items[:, 3]).max()),
+                "achieved_GBps": round(ab["attn"] / (ms * 1e-3) / 1e9, 1)}
+        entry["speedup"] = round(entry["whole_rows"]["ms"] / entry["split_kv"]["ms"], 3)
+        results.append(entry)
+        del q, kn, vn, kc, vc, out
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "attention launch time on straggler batches, whole rows vs split-KV", "unit": "ms",
+                      "higher_is_better": False, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+                      "data": "synthetic", "cache": "cold (512 MiB read sweep before each launch)",
+                      "results": results}))
 
 
 def refresh_bench(args):
@@ -1339,6 +1432,8 @@ def main():
                     help="time the dual-cache refresh (rotated K/V scatter + full-row attention) of one layer; "
                          "with --serve, rebuild the dual cache at every block start of the serving loop")
     ap.add_argument("--no-library", action="store_true", help="--refresh: skip the library attention comparison")
+    ap.add_argument("--stragglers", action="store_true",
+                    help="attention on straggler batches (a few very long rows): whole rows vs split-KV")
     ap.add_argument("--prefix-only", action="store_true",
                     help="prefix-cache layout: keys end at the active block (no masked suffix)")
     args = ap.parse_args()
@@ -1362,6 +1457,13 @@ def main():
                   file=sys.stderr, flush=True)
             sys.exit(2)
         churn_bench(args)
+        return
+    if args.stragglers:
+        if args.gpus != 1:
+            print("bench.py measures one GPU: the attention runs on a single device (run with --gpus 1)",
+                  file=sys.stderr, flush=True)
+            sys.exit(2)
+        stragglers_bench(args)
         return
     if args.refresh and not (args.traffic_summary or args.counter_summary) and not args.serve:
         if args.gpus != 1:

@@ -756,71 +756,75 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_group(AttnArgs a) {
   attn_item<D, 64, NS, true, NI, 0>(a, a.items[blockIdx.x], lds, blockDim.x >> 6, w, threadIdx.x & 63);
 }
 
-// Split-KV merge: one wave per (split row, wave slot wg of its pieces'
-// workgroups), serving the same query head (kvh * G + wg / RBW) and 32 block
-// rows (row block rb + wg % RBW) as those waves. Lane (g, n) folds the
-// pieces' partials of its query column in order, keeping a running max m:
-// the sums so far are scaled by 2^(m_old - m) and piece p's by 2^(m_p - m)
-// (the log-sum-exp merge of softmax pieces); the quotient is written like the
-// attention's own output (bf16; rows B .. L - 1 as zeros). The next piece's
-// loads are issued before the current one is folded.
+// Split-KV merge. Wave (r, wg, k) combines group k (4 of the lane's output
+// features) of split row r for wave slot wg of its pieces' workgroups, which
+// serve query head kvh * G + wg / RBW and 32 block rows (row block
+// rb + wg % RBW). Lane (g, n) folds the pieces' partials of its query column
+// with a running max m: the sums so far are scaled by 2^(m_old - m) and piece
+// p's by 2^(m_p - m) (the log-sum-exp merge of softmax pieces), eight pieces'
+// loads in flight at a time; the quotient is written like the attention's own
+// output (bf16; rows B .. L - 1 as zeros). Every load of a wave is one
+// contiguous 256 B or 1 KiB run.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
   constexpr int NG = D / 8;                       // groups of 4 floats per lane
   constexpr int OFL = NG * 64 * 4;
+  constexpr int CH = 8;                           // pieces per batch of loads
   const int GW = a.G * a.RBW;
-  const int idx = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (idx >= a.n_merge * GW) return;
-  const int wg = idx % GW;
-  const AttnMerge mg = a.merges[idx / GW];
+  const int wv = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (wv >= a.n_merge * GW * NG) return;
+  const int k = wv % NG, wg = (wv / NG) % GW;
+  const AttnMerge mg = a.merges[wv / (NG * GW)];
   const int g = lane >> 5, n = lane & 31;
   const int h = mg.kvh * a.G + wg / a.RBW;
   const int j = (mg.rb + wg % a.RBW) * 32 + n;
   const int64_t pstride = (int64_t)GW * part_wave_floats(D);
   const float* pw = a.parts + ((int64_t)mg.part0 * GW + wg) * part_wave_floats(D);
-  f32x4_t cur[NG], nxt[NG], acc[NG];
-  float cm = pw[OFL + lane], cl = pw[OFL + 64 + lane], nm = 0.0f, nl = 0.0f;
-#pragma unroll
-  for (int k = 0; k < NG; ++k) {
-    cur[k] = *reinterpret_cast<const f32x4_t*>(pw + (k * 64 + lane) * 4);
-    acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  }
+  f32x4_t acc = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   float m = -__builtin_inff(), l = 0.0f;
-  for (int p = 0; p < mg.nparts; ++p) {
-    if (p + 1 < mg.nparts) {
-      const float* pn = pw + (p + 1) * pstride;
-      nm = pn[OFL + lane];
-      nl = pn[OFL + 64 + lane];
+  for (int p0 = 0; p0 < mg.nparts; p0 += CH) {
+    float mp[CH], lp[CH];
+    f32x4_t op[CH];
 #pragma unroll
-      for (int k = 0; k < NG; ++k) nxt[k] = *reinterpret_cast<const f32x4_t*>(pn + (k * 64 + lane) * 4);
+    for (int i = 0; i < CH; ++i) {
+      if (p0 + i < mg.nparts) {
+        const float* pp = pw + (p0 + i) * pstride;
+        mp[i] = pp[OFL + lane];
+        lp[i] = pp[OFL + 64 + lane];
+        op[i] = *reinterpret_cast<const f32x4_t*>(pp + (k * 64 + lane) * 4);
+      } else {
+        mp[i] = -__builtin_inff();
+        lp[i] = 0.0f;
+        op[i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      }
     }
-    const float mn = fmaxf(m, cm);
-    const float sa = __builtin_amdgcn_exp2f(m - mn), sb = __builtin_amdgcn_exp2f(cm - mn);
-    l = fmaf(l, sa, cl * sb);
+    float mn = m;
 #pragma unroll
-    for (int k = 0; k < NG; ++k) acc[k] = acc[k] * sa + cur[k] * sb;
+    for (int i = 0; i < CH; ++i) mn = fmaxf(mn, mp[i]);
+    const float sa = __builtin_amdgcn_exp2f(m - mn);
+    l *= sa;
+    acc *= sa;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const float sb = __builtin_amdgcn_exp2f(mp[i] - mn);     // 0 for the padding entries
+      l = fmaf(lp[i], sb, l);
+      acc += op[i] * sb;
+    }
     m = mn;
-    cm = nm;
-    cl = nl;
-#pragma unroll
-    for (int k = 0; k < NG; ++k) cur[k] = nxt[k];
   }
   if (j >= a.L) return;
   const float inv = j < mg.B ? 1.0f / l : 0.0f;
-  uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)mg.req * a.L + j) * a.Hq + h) * D + 4 * g;
+  // group k = 4 dt + rq holds features 32 dt + 8 rq + 4 g .. + 3
+  uint16_t* op = static_cast<uint16_t*>(a.out) + (((int64_t)mg.req * a.L + j) * a.Hq + h) * D +
+                 32 * (k >> 2) + 8 * (k & 3) + 4 * g;
   typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+  uint32_t w2[2];
 #pragma unroll
-  for (int k = 0; k < NG; ++k) {
-    // group k = 4 dt + rq holds features 32 dt + 8 rq + 4 g .. + 3
-    const int d = 32 * (k >> 2) + 8 * (k & 3);
-    uint32_t w2[2];
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const __bf16 lo = (__bf16)(acc[k][2 * e] * inv), hi = (__bf16)(acc[k][2 * e + 1] * inv);
-      w2[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-    }
-    __builtin_nontemporal_store(v2u{w2[0], w2[1]}, reinterpret_cast<v2u*>(op + d));
+  for (int e = 0; e < 2; ++e) {
+    const __bf16 lo = (__bf16)(acc[2 * e] * inv), hi = (__bf16)(acc[2 * e + 1] * inv);
+    w2[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
   }
+  __builtin_nontemporal_store(v2u{w2[0], w2[1]}, reinterpret_cast<v2u*>(op));
 }
 
 template <int D>
@@ -834,7 +838,7 @@ hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
     hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 4>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   }
   if (GW > 1 && a.n_merge > 0)
-    hipLaunchKernelGGL((k_attn_merge<D>), dim3((a.n_merge * GW + 3) / 4), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_attn_merge<D>), dim3((a.n_merge * GW * (D / 8) + 3) / 4), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -191,6 +191,24 @@ def workload(cfg: int, variant: int = 0, block_length: int | None = None, **over
     return w
 
 
+def straggler(case: int) -> Workload:
+    """Dream-7B-shaped GQA batches (28 query / 4 KV heads, D = 128, L = 32,
+    g = 512, p ~ U[128, 1024)) with a few rows far longer than the rest, the
+    straggler mix a heterogeneous serving batch can hold: case 0 is 24
+    requests with one prompt of 8000 tokens; case 1 is 64 requests with
+    prompts of 16000 and 6000 tokens."""
+    r = rng(200 + case, 0, S_DESC)
+    n, longs = ((24, {8: 8000}), (64, {5: 16000, 40: 6000}))[case]
+    p = r.integers(128, 1024, n)
+    for i, v in longs.items():
+        p[i] = v
+    k = r.integers(0, 16, n)
+    w = custom(32, 28, 4, 128, 152064, "bf16", p.tolist(), [512] * n, k.tolist(), cfg=200 + case,
+               kv_sigma=1.0 / np.sqrt(128.0))
+    w.name = f"dream7b-stragglers-n{n}-" + "-".join(str(v) for v in longs.values()) + "-gqa28x4-d128-L32"
+    return w
+
+
 def custom(L, Hq, Hkv, D, V, dtype, p, g, k, *, W=None, rows=None, R=None, cfg=100, variant=0,
            tau=0.9, q_min=1, eos_id=-1, layers=1, q_sigma=1.0, kv_sigma=1.0, logits="spiked",
            logit_sigma=1.0) -> Workload:

@@ -505,6 +505,10 @@ def counter_summary(args, workload):
             keep.append(f"`counters {pref} {hashes[pref] if hashes is not None else source_hash(pref)}`")
     lines += ["", f"Sources of each library kernel ({hash_note(hashes)}; a changed kernel makes the row",
               "stale):", ""] + [k + "  " for k in sorted(set(keep))] + [""]
+    if any(r.startswith("| `hipBLASLt") for r in lines):
+        lines += ["The `hipBLASLt GEMM` row is the library GEMM (torch.matmul) that the bench's unfused",
+                  "comparison runs in the same process on the same rows (no source hash: not this library's code).",
+                  ""]
     open(os.path.join(ROOT, "profiles", f"counters_{workload}.md"), "w").write("\n".join(lines))
     print("\n".join(lines))
 

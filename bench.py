@@ -795,7 +795,7 @@ def lm_head_bench(args):
 
 def stragglers_bench(args):
     """Attention of one layer on straggler batches (synth.straggler: a few rows
-    far longer than the rest of a Dream-7B-shaped batch), whole rows against
+    far longer than the rest of a Dream-7B- or LLaDA-8B-shaped batch), whole rows against
     the split-KV plan. Each launch is bracketed by HIP events on its stream,
     enqueued behind a 512 MiB read sweep (so the host call overlaps the sweep
     and the region holds the launch alone, with a cold Infinity Cache).
@@ -816,7 +816,7 @@ def stragglers_bench(args):
         return x.to(torch.bfloat16)
 
     results = []
-    for case in (0, 1):
+    for case in (0, 1, 2):
         w = synth.straggler(case)
         print(f"[bench] stragglers: {w.name}", file=sys.stderr, flush=True)
         q = draw((w.n, w.L, w.Hq, w.D), 1.0)

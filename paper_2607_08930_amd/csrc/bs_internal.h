@@ -34,11 +34,10 @@ __device__ inline void st16(void* p, v4u v) { *reinterpret_cast<v4u*>(p) = v; }
 // ---------------------------------------------------------------- attention
 // One work item = (request, KV head) with the request's geometry resolved on
 // the host, so a workgroup needs a single scalar load before its first DMA.
-// In the shared-tile (GQA) kernel an item may be one piece of a row: keys
-// [64 t0, min(64 t1, len)), with its un-normalised output, running max and
-// row sum going to partial slot `part` for a merge launch (split-KV); part
-// < 0 marks a whole row (t0 = 0, t1 = ceil(len / 64)) written out directly.
-// The single-wave (MHA) kernel always takes whole rows and ignores the three.
+// An item may be one piece of a row: keys [64 t0, min(64 t1, len)), with its
+// un-normalised output, running max and row sum going to partial slot `part`
+// for a merge launch (split-KV); part < 0 marks a whole row (t0 = 0,
+// t1 = ceil(len / 64)) written out directly.
 struct AttnItem {
   int32_t req;   // request index (row of q / k_new / v_new / out)
   int32_t kvh;   // KV head

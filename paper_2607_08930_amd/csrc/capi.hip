@@ -341,6 +341,17 @@ size_t attention_item_count(int n, int L, int Hq, int Hkv, bs_dtype dt) {
   return dt == BS_BF16 ? (size_t)n * Hkv * attention_split(L, Hq, Hkv) : 0;
 }
 
+// The single-wave kernel's list (sorted longest first): workgroup b takes
+// items b, b + NB, b + 2 NB, b + 3 NB, so every workgroup holds a long and a
+// short share (only when the list fills whole workgroups).
+void interleave_waves(AttnItem* items, AttnItem* tmp, size_t N) {
+  if (N % kMhaWaves) return;
+  const size_t NB = N / kMhaWaves;
+  for (size_t b = 0; b < NB; ++b)
+    for (size_t j = 0; j < (size_t)kMhaWaves; ++j) tmp[b * kMhaWaves + j] = items[j * NB + b];
+  std::copy(tmp, tmp + N, items);
+}
+
 void attention_items_into(AttnItem* items, AttnItem* tmp, const bs_req_desc* reqs, int n, int L, int Hq, int Hkv) {
   const int split = attention_split(L, Hq, Hkv);
   size_t N = 0;
@@ -358,71 +369,89 @@ void attention_items_into(AttnItem* items, AttnItem* tmp, const bs_req_desc* req
     if (x.kvh != y.kvh) return x.kvh < y.kvh;
     return x.rb < y.rb;
   });
-  if (Hq == Hkv && L <= 32 && N % kMhaWaves == 0) {
-    const size_t NB = N / kMhaWaves;
-    for (size_t b = 0; b < NB; ++b)
-      for (size_t j = 0; j < (size_t)kMhaWaves; ++j) tmp[b * kMhaWaves + j] = items[j * NB + b];
-    std::copy(tmp, tmp + N, items);
-  }
+  if (Hq == Hkv && L <= 32) interleave_waves(items, tmp, N);
 }
 
-// ---- split-KV plan (shared-tile kernel)
-// The shared-tile kernel runs one workgroup per CU (its ring fills the LDS),
-// so a launch of whole rows lasts at least as long as its longest row, while
-// CUs that drew short rows sit idle: the straggler effect of a heterogeneous
-// batch. The plan can cut rows into pieces of 64-key tiles; each piece writes
-// a partial and a merge launch combines a row's pieces. Its estimate of a
-// launch, in tiles of one workgroup's loop, is the larger of
-//  * the list schedule: workgroups longest first on the least-loaded of
-//    kPlanCUs CUs (what the dispatcher does with a list sorted that way),
-//    each costing kPieceOverhead + its tiles, and
-//  * the machine-wide bound: all workgroups' cost over kPlanCUs, times
-//    kFullLoad (a tile takes that much longer when every CU runs the loop
-//    than when few do; measured on the Dream-7B layer: 2.07 against 1.64 us),
+// ---- split-KV plan
+// The attention kernels hold a fixed number of work slots at once: the
+// shared-tile (GQA) kernel one workgroup per CU (its ring fills the LDS), the
+// single-wave (MHA) kernel four waves per CU. So a launch of whole rows lasts
+// at least as long as its longest row, while slots that drew short rows sit
+// idle: the straggler effect of a heterogeneous batch. The plan can cut rows
+// into pieces of 64-key tiles; each piece writes a partial and a merge launch
+// combines a row's pieces. Its estimate of a launch, in 64-key tiles of one
+// slot's loop, is the larger of
+//  * the list schedule: work items longest first on the least-loaded slot
+//    (what the dispatcher does with a list sorted that way), each costing
+//    kPieceOverhead + its tiles, and
+//  * the machine-wide bound: all items' cost over the slots, times the
+//    kernel's full-load factor (a tile takes that much longer when every slot
+//    runs the loop than when few do: measured 2.07 against 1.64 us on the
+//    Dream-7B layer for the shared-tile kernel; the single-wave kernel streams
+//    memory, about 4.8 GB/s per wave when all 1024 run and several times that
+//    alone, and 2.0 picked the faster of the caps tried on an LLaDA-8B batch
+//    with one 16000-token prompt: 17 tiles, 130 us, against 22 tiles, 139 us,
+//    with 3.0),
 // plus, when anything is cut, the merge launch. Targets T just above the
 // balanced load are tried: a row longer than T - kPieceOverhead tiles is cut
 // into pieces of that many tiles plus the rest. The lowest estimate wins;
 // with none below the whole rows' estimate nothing is cut. So a batch that
 // fills the GPU with rows of similar length runs whole, and a few long rows
-// beside short ones are spread over the idle CUs.
+// beside short ones are spread over the idle slots.
 constexpr int kPlanCUs = 256;
 constexpr double kPieceOverhead = 2.0;
-constexpr double kFullLoad = 1.3;
 constexpr double kMergeFixed = 3.0;        // the merge launch, in tiles
 constexpr double kMergePerPart = 0.02;     // per partial read back
 
+struct PlanShape {
+  int group;          // work items per workgroup (one workgroup per CU)
+  double full_load;   // per-tile slowdown with every slot busy
+};
+
 bool shared_tile_path(int L, int Hq, int Hkv) { return !(Hq == Hkv && L <= 32); }
+
+PlanShape plan_shape(int L, int Hq, int Hkv) {
+  return shared_tile_path(L, Hq, Hkv) ? PlanShape{1, 1.3} : PlanShape{kMhaWaves, 2.0};
+}
 
 int waves_per_item(int L, int Hq, int Hkv) {
   const int G = Hq / Hkv, RB = (L + 31) / 32;
   return G * (G * RB > 8 ? 1 : RB);
 }
 
-// Estimated launch time (tiles) of workgroups of `tiles` tiles each (sorts `tiles`).
-double launch_estimate(std::vector<int>& tiles) {
+// Estimated launch time (tiles) of work items of `tiles` tiles each (sorts
+// `tiles`). Items go to workgroups as the launch will place them (a group of
+// ps.group items, interleaved like interleave_waves when they fill whole
+// workgroups); a workgroup holds its CU until its longest item is done.
+double launch_estimate(std::vector<int>& tiles, const PlanShape& ps) {
   std::sort(tiles.begin(), tiles.end(), std::greater<int>());
+  const size_t N = tiles.size(), G = (size_t)ps.group;
+  const size_t NB = (N + G - 1) / G;
+  double total = 0.0;
+  for (int t : tiles) total += kPieceOverhead + t;
   std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
   for (int i = 0; i < kPlanCUs; ++i) cu.push(0.0);
-  double end = 0.0, total = 0.0;
-  for (int t : tiles) {
-    const double x = cu.top() + kPieceOverhead + t;
+  double end = 0.0;
+  for (size_t b = 0; b < NB; ++b) {
+    // sorted list: the workgroup's longest item is its first
+    const int longest = N % G == 0 ? tiles[b] : tiles[b * G];
+    const double x = cu.top() + kPieceOverhead + longest;
     cu.pop();
     cu.push(x);
     end = std::max(end, x);
-    total += kPieceOverhead + t;
   }
-  return std::max(end, kFullLoad * total / kPlanCUs);
+  return std::max(end, ps.full_load * total / ((double)kPlanCUs * G));
 }
 
 // Largest piece (tiles) of the best plan for rows of nt[i] tiles, or 0 for no cut.
-int split_cap(const std::vector<int>& nt) {
+int split_cap(const std::vector<int>& nt, const PlanShape& ps) {
   if (nt.empty()) return 0;
   double total = 0.0;
   for (int t : nt) total += t + kPieceOverhead;
   std::vector<int> w(nt);
-  const double whole = launch_estimate(w);
-  const int lb = (int)std::ceil(total / kPlanCUs);
-  if (whole <= kFullLoad * lb + kMergeFixed) return 0;    // no plan can gain
+  const double whole = launch_estimate(w, ps);
+  const int lb = (int)std::ceil(total / ((double)kPlanCUs * ps.group));
+  if (whole <= ps.full_load * lb + kMergeFixed) return 0;    // no plan can gain
   double best = whole;
   int best_cap = 0;
   for (int T = lb; T <= lb + 5; ++T) {
@@ -438,7 +467,7 @@ int split_cap(const std::vector<int>& nt) {
       for (int r = t; r > 0; r -= cap) w.push_back(std::min(r, cap));
       parts += (t + cap - 1) / cap;
     }
-    const double est = launch_estimate(w) + kMergeFixed + kMergePerPart * parts;
+    const double est = launch_estimate(w, ps) + kMergeFixed + kMergePerPart * parts;
     if (est < best) {
       best = est;
       best_cap = cap;
@@ -493,14 +522,18 @@ void attention_blob(Blob& blob, const bs_req_desc* reqs, int n, int L, int Hq, i
     std::vector<AttnItem> items(N), tmp(N);
     attention_items_into(items.data(), tmp.data(), reqs, n, L, Hq, Hkv);
     int cap = 0;
-    if (split && shared_tile_path(L, Hq, Hkv)) {
+    if (split) {
       std::vector<int> nt(N);
       for (size_t i = 0; i < N; ++i) nt[i] = items[i].t1 - items[i].t0;
-      cap = split_cap(nt);
+      cap = split_cap(nt, plan_shape(L, Hq, Hkv));
     }
     std::vector<AttnItem> pieces;
     std::vector<AttnMerge> merges;
     const int parts = cap > 0 ? split_items(items, cap, pieces, merges) : 0;
+    if (cap > 0 && !shared_tile_path(L, Hq, Hkv)) {
+      std::vector<AttnItem> t2(pieces.size());
+      interleave_waves(pieces.data(), t2.data(), pieces.size());
+    }
     const std::vector<AttnItem>& list = cap > 0 ? pieces : items;
     blob.meta[1] = (int)blob.add(list.data(), sizeof(AttnItem) * list.size());
     blob.meta[2] = (int)list.size();
@@ -872,15 +905,14 @@ int bs_scatter_active_blocks_n(bs_ctx* c, const bs_req_desc* reqs, int n, int L,
 // ------------------------------------------------------------------ K2
 size_t bs_attention_workspace_bytes(const bs_req_desc* reqs, int n, int L, int Hq, int Hkv, int D,
                                     bs_dtype dt) {
-  if (!reqs || n <= 0 || dt != BS_BF16 || L < 1 || L > 64 || Hkv < 1 || Hq < Hkv || Hq % Hkv || (D != 64 && D != 128) ||
-      !shared_tile_path(L, Hq, Hkv))
+  if (!reqs || n <= 0 || dt != BS_BF16 || L < 1 || L > 64 || Hkv < 1 || Hq < Hkv || Hq % Hkv || (D != 64 && D != 128))
     return 0;
   const size_t N = attention_item_count(n, L, Hq, Hkv, dt);
   std::vector<AttnItem> items(N), tmp(N);
   attention_items_into(items.data(), tmp.data(), reqs, n, L, Hq, Hkv);
   std::vector<int> nt(N);
   for (size_t i = 0; i < N; ++i) nt[i] = std::max(items[i].t1 - items[i].t0, 0);
-  const int cap = split_cap(nt);
+  const int cap = split_cap(nt, plan_shape(L, Hq, Hkv));
   int parts = 0;
   if (cap > 0)
     for (int t : nt)

@@ -318,10 +318,11 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
       }
     }
   };
-  // tiles of this item: the whole row, or (shared-tile kernel) one piece of
-  // it, keys [tb0, tb0 + ntiles * KT) clamped to the row
-  const int tb0 = SHARED ? it.t0 * KT : 0;
-  const int ntiles = SHARED ? it.t1 - it.t0 : (len + KT - 1) / KT;
+  // tiles of this item: keys [64 t0, min(64 t1, len)) of the row (the whole
+  // row, or one piece of it), in KT-key tiles from tb0
+  constexpr int TPU = kAttnTile / KT;             // KT-key tiles per 64-key unit
+  const int tb0 = it.t0 * kAttnTile;
+  const int ntiles = min((len + KT - 1) / KT, it.t1 * TPU) - it.t0 * TPU;
   // The request's block mask word, in the fused step (one item per request:
   // KV head 0, first row block, its first wave): lane j reads mask cell j of
   // the block, by inline assembly so the compiler adds no wait of its own;
@@ -568,7 +569,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     for (int tile = 0; tile < ntiles; ++tile) {
       const int nxt = tile + NS - 1;
       const bool ahead = nxt < ntiles;
-      if (ahead) issue(nxt % NS, nxt * KT);
+      if (ahead) issue(nxt % NS, tb0 + nxt * KT);
       // this tile's stage has landed once only the next stage's DMA (if
       // issued) and the previous tile's stores (if any) remain
       if (ahead) {
@@ -584,7 +585,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
       }
       const uint16_t* kt = ring + (tile % NS) * STAGE;
       const uint16_t* vtl = kt + TILE;
-      const int tb = tile * KT;
+      const int tb = tb0 + tile * KT;
   #pragma unroll
       for (int sub = 0; sub < KT / 32; ++sub) {
         const int sb = tb + sub * 32;
@@ -666,9 +667,7 @@ __device__ inline void attn_item(const AttnArgs& a, const AttnItem it, uint16_t*
     }
   }
   const float lt = xhalf_sum(lsum);
-  bool whole = true;
-  if constexpr (SHARED) whole = it.part < 0;
-  if (!whole) {
+  if (it.part >= 0) {
     // One piece of a split row: the un-normalised O^T (accumulator order,
     // whole 16-byte groups per lane), the running max in log2 units and the
     // row sum go to the piece's partial slot for the merge launch.
@@ -837,7 +836,7 @@ hipError_t launch_bf16_d(const AttnArgs& a, int GW, hipStream_t s) {
   } else {
     hipLaunchKernelGGL((k_attn_bf16_group<D, 4, 4>), dim3(a.n_items), dim3(64 * GW), 0, s, a);
   }
-  if (GW > 1 && a.n_merge > 0)
+  if (a.n_merge > 0)
     hipLaunchKernelGGL((k_attn_merge<D>), dim3((a.n_merge * GW * (D / 8) + 3) / 4), dim3(256), 0, s, a);
   return hipGetLastError();
 }

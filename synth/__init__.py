@@ -192,20 +192,28 @@ def workload(cfg: int, variant: int = 0, block_length: int | None = None, **over
 
 
 def straggler(case: int) -> Workload:
-    """Dream-7B-shaped GQA batches (28 query / 4 KV heads, D = 128, L = 32,
-    g = 512, p ~ U[128, 1024)) with a few rows far longer than the rest, the
-    straggler mix a heterogeneous serving batch can hold: case 0 is 24
-    requests with one prompt of 8000 tokens; case 1 is 64 requests with
-    prompts of 16000 and 6000 tokens."""
+    """Batches with a few rows far longer than the rest, the straggler mix a
+    heterogeneous serving batch can hold. Cases 0 and 1 are Dream-7B-shaped
+    (28 query / 4 KV heads, D = 128, L = 32, g = 512, p ~ U[128, 1024)): 24
+    requests with one prompt of 8000 tokens, and 64 requests with prompts of
+    16000 and 6000 tokens. Case 2 is LLaDA-8B-shaped (32 MHA heads, D = 128,
+    L = 32, g = 256, p ~ U[64, 512)): 32 requests with one prompt of 16000
+    tokens."""
     r = rng(200 + case, 0, S_DESC)
-    n, longs = ((24, {8: 8000}), (64, {5: 16000, 40: 6000}))[case]
-    p = r.integers(128, 1024, n)
+    if case == 2:
+        n, longs, lo, hi, g, Hq, Hkv, V, K = 32, {7: 16000}, 64, 512, 256, 32, 32, 126464, 8
+        tag = "llada8b", "mha32"
+    else:
+        n, longs = ((24, {8: 8000}), (64, {5: 16000, 40: 6000}))[case]
+        lo, hi, g, Hq, Hkv, V, K = 128, 1024, 512, 28, 4, 152064, 16
+        tag = "dream7b", "gqa28x4"
+    p = r.integers(lo, hi, n)
     for i, v in longs.items():
         p[i] = v
-    k = r.integers(0, 16, n)
-    w = custom(32, 28, 4, 128, 152064, "bf16", p.tolist(), [512] * n, k.tolist(), cfg=200 + case,
+    k = r.integers(0, K, n)
+    w = custom(32, Hq, Hkv, 128, V, "bf16", p.tolist(), [g] * n, k.tolist(), cfg=200 + case,
                kv_sigma=1.0 / np.sqrt(128.0))
-    w.name = f"dream7b-stragglers-n{n}-" + "-".join(str(v) for v in longs.values()) + "-gqa28x4-d128-L32"
+    w.name = f"{tag[0]}-stragglers-n{n}-" + "-".join(str(v) for v in longs.values()) + f"-{tag[1]}-d128-L32"
     return w
 
 

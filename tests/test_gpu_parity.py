@@ -480,8 +480,9 @@ def test_attention_split_kv_matches_whole_rows(ctx):
 def test_attention_split_kv_stragglers(ctx):
     # one or two rows far longer than the rest of a small batch: the plan cuts
     # them into many pieces (several partials per merged row), also with two
-    # row blocks per workgroup (L = 64, G = 4, D = 64) and one row block per
-    # workgroup (L = 64, G = 7), and with the fresh block inside a cut piece
+    # row blocks per workgroup (L = 64, G = 4, D = 64), one row block per
+    # workgroup (L = 64, G = 7) and the single-wave MHA kernel, and with the
+    # fresh block inside a cut piece
     _, bs, _ = lazy()
     rng = np.random.default_rng(5)
     cases = [
@@ -489,6 +490,8 @@ def test_attention_split_kv_stragglers(ctx):
         ("G4 L64 D64", 64, 8, 2, 64, 5000, 30),
         ("G7 L64 D128", 64, 28, 4, 128, 3000, 12),
         ("G2 L32 D128", 32, 4, 2, 128, 9000, 60),
+        ("MHA L32 D128", 32, 32, 32, 128, 12000, 32),
+        ("MHA L32 D64", 32, 8, 8, 64, 7000, 20),
     ]
     for label, L, Hq, Hkv, D, long_p, n in cases:
         p = rng.integers(16, 300, n)

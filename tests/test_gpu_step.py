@@ -134,6 +134,48 @@ def test_fused_step_block_length_sweep(ctx, cfg, L):
     assert stats.band <= max(4, stats.positions // 50), stats
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(28, 4), (8, 8)])
+def test_fused_step_split_kv_stragglers(ctx, Hq, Hkv):
+    """A small batch with one long row, two layers: the fused step runs the
+    split-KV plan (partial slots after the decode's part of its workspace)
+    and matches the oracle; it equals the separate calls given the same
+    workspace byte for byte, and the whole-row step within the attention
+    bound (decode outputs identical)."""
+    torch, bs, bstep = lazy()
+    g_ = np.random.default_rng(77)
+    n = 12
+    p = g_.integers(40, 400, n)
+    p[4] = 3000
+    gen = np.full(n, 96)
+    k = g_.integers(0, 3, n)
+    w = synth.custom(32, Hq, Hkv, 128, 2048, "bf16", list(p), list(gen), list(k), variant=3, layers=2,
+                     kv_sigma=128 ** -0.5)
+    items, parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
+    say(f"[fused step split-KV G={Hq // Hkv}] n={n} W={w.W}: {len(items)} work items, {parts} partial slots")
+    assert parts > 0
+    a, host = make_state(w)
+    b, _ = make_state(w)
+    c, _ = make_state(w)
+    bstep.run_step(ctx, a, w.reqs, want_conf=True, fused=True)
+    bstep.run_step(ctx, b, w.reqs, want_conf=True, fused=False)
+    bstep.run_step(ctx, c, w.reqs, want_conf=True, fused=True, split=False)
+    torch.cuda.synchronize()
+    ga, gb, gc = snapshot(a), snapshot(b), snapshot(c)
+    ref = oracle.mixed_state_step(w.reqs, w.L, host["tokens"], host["mask"], host["layers"], host["logits"],
+                                  tau=w.tau, q_min=w.q_min, eos_id=w.eos_id, dtype=w.dtype)
+    stats = check_step(w, ga, ref, host, f"split-KV G={Hq // Hkv}")
+    say(f"  decode: {stats}")
+    for key in ("tokens", "mask", "pos", "conf", "n_unmasked", "done", "eos_seen"):
+        np.testing.assert_array_equal(ga[key], gb[key], err_msg=key)
+        np.testing.assert_array_equal(ga[key], gc[key], err_msg=key)
+    for la, lb, lc in zip(ga["layers"], gb["layers"], gc["layers"]):
+        for key in ("out", "k_cache", "v_cache"):
+            np.testing.assert_array_equal(la[key], lb[key], err_msg=key)
+        np.testing.assert_array_equal(la["k_cache"], lc["k_cache"])
+        np.testing.assert_array_equal(la["v_cache"], lc["v_cache"])
+        check_attention(w, la["out"], oracle.widen(lc["out"], w.dtype), label="split vs whole rows")
+
+
 def test_fused_step_equals_separate_calls(ctx):
     """Same kernels, same order: the fused call and the K1/K2/K3/K1^-1
     sequence give identical bytes (GQA shapes, three layers)."""

@@ -521,6 +521,8 @@ def kernel_summary(args):
     import csv
     import glob
     d, name = args.kernel_summary
+    if os.sep in name or name.startswith("."):
+        sys.exit(f"--kernel-summary: NAME must be a plain file stem under profiles/, not {name!r}")
     cmd = args.bench_args
     rows = []
     for fn in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
@@ -544,6 +546,13 @@ def kernel_summary(args):
             steps.setdefault(ka, []).append(((a[1] - a[0]) / 1e3, (b[0] - a[1]) / 1e3, (b[1] - b[0]) / 1e3,
                                              (c[0] - b[1]) / 1e3, (c[1] - c[0]) / 1e3, (c[1] - a[0]) / 1e3))
             tag[b] = tag[c] = f" (step of {ka})"
+            tag[a] = ""
+    if steps:
+        # attention launches of the same run that belong to no step (the
+        # straggler batches of the default run) are listed apart
+        for k in ks:
+            if "k_attn" in k[2] and k not in tag:
+                tag[k] = " (outside a step)"
     per = {}
     for k in ks:
         per.setdefault(short(k[2]) + tag.get(k, ""), []).append((k[1] - k[0]) / 1e3)
@@ -793,71 +802,77 @@ def lm_head_bench(args):
     print(json.dumps(res), flush=True)
 
 
-def stragglers_bench(args):
-    """Attention of one layer on straggler batches (synth.straggler: a few rows
-    far longer than the rest of a Dream-7B- or LLaDA-8B-shaped batch), whole rows against
-    the split-KV plan. Each launch is bracketed by HIP events on its stream,
-    enqueued behind a 512 MiB read sweep (so the host call overlaps the sweep
-    and the region holds the launch alone, with a cold Infinity Cache).
-    Inputs are drawn on the device (queries and fresh K/V ~ N(0, 1), cache ~
-    N(0, 1/D)). Prints one JSON line."""
+def straggler_case(ctx, case, steps, warmup):
+    """Whole rows against the split-KV plan for one straggler batch
+    (synth.straggler(case)): the attention launch bracketed by HIP events on
+    its stream, enqueued behind a 512 MiB read sweep (so the host call
+    overlaps the sweep and the region holds the launch alone, with a cold
+    Infinity Cache). Inputs are drawn on the device (queries and fresh K/V ~
+    N(0, 1), cache ~ N(0, 1/D)). Returns the batch's record."""
     import torch
     import synth
     import paper_2607_08930_amd as bs
 
-    torch.cuda.set_device(0)
-    ctx = bs.Context(0)
     stream = torch.cuda.current_stream()
     flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
-    gen = torch.Generator(device="cuda").manual_seed(7)
+    gen = torch.Generator(device="cuda").manual_seed(7 + case)
 
     def draw(shape, sigma):
         x = torch.empty(shape, dtype=torch.float32, device="cuda").normal_(0.0, sigma, generator=gen)
         return x.to(torch.bfloat16)
 
-    results = []
-    for case in (0, 1, 2):
-        w = synth.straggler(case)
-        print(f"[bench] stragglers: {w.name}", file=sys.stderr, flush=True)
-        q = draw((w.n, w.L, w.Hq, w.D), 1.0)
-        kn, vn = draw((w.n, w.L, w.Hkv, w.D), 1.0), draw((w.n, w.L, w.Hkv, w.D), 1.0)
-        kc, vc = draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5), draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5)
-        out = torch.empty_like(q)
-        torch.cuda.synchronize()
-        ab = algorithmic_bytes(w)
-        lens = w.reqs["p"] + w.reqs["g"]
-        entry = {"workload": w.name, "n_requests": int(w.n), "max_len": int(lens.max()), "sum_len": int(lens.sum()),
-                 "algorithmic_bytes": int(ab["attn"])}
-        for split in (False, True):
-            nws = bs.bs_attention_workspace_bytes(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16) if split else 0
-            ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    w = synth.straggler(case)
+    print(f"[bench] stragglers: {w.name}", file=sys.stderr, flush=True)
+    q = draw((w.n, w.L, w.Hq, w.D), 1.0)
+    kn, vn = draw((w.n, w.L, w.Hkv, w.D), 1.0), draw((w.n, w.L, w.Hkv, w.D), 1.0)
+    kc, vc = draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5), draw((w.R, w.Hkv, w.W, w.D), w.D ** -0.5)
+    out = torch.empty_like(q)
+    torch.cuda.synchronize()
+    ab = algorithmic_bytes(w)
+    lens = w.reqs["p"] + w.reqs["g"]
+    entry = {"workload": w.name, "n_requests": int(w.n), "max_len": int(lens.max()), "sum_len": int(lens.sum()),
+             "algorithmic_bytes": int(ab["attn"])}
+    for split in (False, True):
+        nws = bs.bs_attention_workspace_bytes(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16) if split else 0
+        ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
 
-            def call():
-                bs.bs_dual_cache_block_attention(ctx, w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 0.0, q, kn, vn,
-                                                 kc, vc, w.R, w.W, 1, out, ws if nws else None, nws,
-                                                 stream=stream)
+        def call():
+            bs.bs_dual_cache_block_attention(ctx, w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 0.0, q, kn, vn,
+                                             kc, vc, w.R, w.W, 1, out, ws if nws else None, nws, stream=stream)
 
-            for _ in range(args.warmup):
-                call()
-            ts = []
-            for _ in range(args.steps):
-                flush.sum()
-                e0, e1 = region_events()
-                e0.record(stream)
-                call()
-                e1.record(stream)
-                torch.cuda.synchronize()
-                ts.append(e0.elapsed_time(e1))
-            items, parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, int(split))
-            ms = float(np.median(ts))
-            entry["split_kv" if split else "whole_rows"] = {
-                "ms": round(ms, 5), "workgroups": int(len(items)), "partial_slots": int(parts),
-                "longest_workgroup_tiles": int((items[:, 4] - items[:, 3]).max()),
-                "achieved_GBps": round(ab["attn"] / (ms * 1e-3) / 1e9, 1)}
-        entry["speedup"] = round(entry["whole_rows"]["ms"] / entry["split_kv"]["ms"], 3)
-        results.append(entry)
-        del q, kn, vn, kc, vc, out
-        torch.cuda.empty_cache()
+        for _ in range(warmup):
+            call()
+        ts = []
+        for _ in range(steps):
+            flush.sum()
+            e0, e1 = region_events()
+            e0.record(stream)
+            call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        items, parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, int(split))
+        ms = float(np.median(ts))
+        entry["split_kv" if split else "whole_rows"] = {
+            "ms": round(ms, 5), "workgroups": int(len(items)), "partial_slots": int(parts),
+            "longest_workgroup_tiles": int((items[:, 4] - items[:, 3]).max()),
+            "achieved_GBps": round(ab["attn"] / (ms * 1e-3) / 1e9, 1)}
+    entry["speedup"] = round(entry["whole_rows"]["ms"] / entry["split_kv"]["ms"], 3)
+    del q, kn, vn, kc, vc, out, flush
+    torch.cuda.empty_cache()
+    return entry
+
+
+def stragglers_bench(args):
+    """Attention of one layer on straggler batches (synth.straggler: a few rows
+    far longer than the rest of a Dream-7B- or LLaDA-8B-shaped batch), whole
+    rows against the split-KV plan (straggler_case). Prints one JSON line."""
+    import torch
+    import paper_2607_08930_amd as bs
+
+    torch.cuda.set_device(0)
+    ctx = bs.Context(0)
+    results = [straggler_case(ctx, case, args.steps, args.warmup) for case in (0, 1, 2)]
     print(json.dumps({"metric": "attention launch time on straggler batches, whole rows vs split-KV", "unit": "ms",
                       "higher_is_better": False, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
                       "data": "synthetic", "cache": "cold (512 MiB read sweep before each launch)",
@@ -1513,6 +1528,10 @@ def main():
                                                        "ms_per_step_warm", "ms_per_step_with_flag_readback", "copy_reference",
                                                        "parity", "cpu_baseline")
                                 if k in second}
+        # straggler handling (split-KV) on the LLaDA-8B-shaped batch with one
+        # 16000-token prompt: whole rows against the plan, attention only
+        import paper_2607_08930_amd as bs
+        res["straggler_split_kv"] = straggler_case(bs.Context(0), 2, 10, 2)
     print(json.dumps(res), flush=True)
 
 

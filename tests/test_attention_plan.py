@@ -127,3 +127,35 @@ def test_plan_is_a_function_of_the_descriptors():
     a = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
     b = bs.bs_attention_work_list(w.reqs.copy(), w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
     assert np.array_equal(a[0], b[0]) and a[1] == b[1]
+
+
+def test_plan_edge_cases():
+    # one request: a short row stays whole; a 20000-key row alone is cut into
+    # pieces that spread it over the CUs, every piece within the cap
+    for Hq, Hkv in [(28, 4), (32, 32)]:
+        w = synth.custom(32, Hq, Hkv, 128, 10, "bf16", [10], [20], [0])
+        items, n_parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
+        assert n_parts == 0 and len(items) == Hkv
+        w = synth.custom(32, Hq, Hkv, 128, 10, "bf16", [20000], [64], [1])
+        items, n_parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
+        _check_plan(w, items, n_parts)
+        assert n_parts == len(items) and len(items) >= 4 * Hkv
+        for h in range(Hkv):
+            row = sorted((int(a), int(b)) for r, kv, rb, a, b, part in items.tolist() if kv == h)
+            sizes = [b - a for a, b in row]
+            # pieces of the cap, then the rest
+            assert len(set(sizes[:-1])) == 1 and 0 < sizes[-1] <= sizes[0], sizes
+    # rows shorter than one tile, and a batch with an empty work list (f32)
+    w = synth.custom(32, 8, 2, 64, 10, "bf16", [0, 3, 5000], [1, 30, 32], [0, 0, 0])
+    items, n_parts = bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_BF16, 1)
+    _check_plan(w, items, n_parts)
+    assert bs.bs_attention_workspace_bytes(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_F32) == 0
+
+
+def test_work_list_rejects_unsupported_shapes():
+    import pytest
+    w = synth.custom(32, 8, 2, 128, 10, "bf16", [10], [20], [0])
+    with pytest.raises(bs.BlockServeError):
+        bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, w.D, bs.BS_F32, 1)
+    with pytest.raises(bs.BlockServeError):
+        bs.bs_attention_work_list(w.reqs, w.L, w.Hq, w.Hkv, 96, bs.BS_BF16, 1)

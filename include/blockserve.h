@@ -181,13 +181,15 @@ int bs_scatter_active_blocks_n(bs_ctx* ctx, const bs_req_desc* reqs, int n, int 
  * stale block slot are never read (they may hold NaN).
  * ws: NULL, or a device workspace of ws_bytes bytes (contents on entry
  * ignored). Straggler handling (split-KV; the paper's straggler effect,
- * Introduction and RQ2): the BS_BF16 kernel with G * ceil(L / 32) >= 2 waves
- * per row runs one workgroup per CU, so a batch of whole rows lasts as long
- * as its longest row. bs_attention_workspace_bytes(...) returns the bytes of
- * partial slots for a plan that cuts the longest rows into pieces of 64-key
- * tiles (each piece writes its un-normalised output, running max and row sum;
- * a merge launch combines them by log-sum-exp weights), or 0 when no cut pays
- * off (balanced rows, MHA with L <= 32, BS_F32, invalid arguments). With
+ * Introduction and RQ2): the BS_BF16 kernels hold a fixed number of rows at
+ * once (one workgroup of G * ceil(L / 32) waves per CU, or four single-wave
+ * rows per CU for MHA with L <= 32), so a batch of whole rows lasts at least
+ * as long as its longest row. bs_attention_workspace_bytes(...) returns the
+ * bytes of partial slots for a plan that cuts the longest rows into pieces of
+ * 64-key tiles (each piece writes its un-normalised output, running max and
+ * row sum; a merge launch combines them by log-sum-exp weights), or 0 when no
+ * cut pays off (rows that already fill the GPU evenly, BS_F32, invalid
+ * arguments). With
  * ws_bytes at least that size the call runs the plan, otherwise every row
  * whole; both agree within rounding (bf16 output). The plan depends only on
  * the arguments of the size query. Calls that may overlap (different

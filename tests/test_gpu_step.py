@@ -85,11 +85,13 @@ def test_fused_step_matches_oracle(ctx, cfg):
     assert stats.band <= max(4, stats.positions // 50), stats
 
 
-@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("seed", range(24))
 def test_fused_step_random_geometries(ctx, seed):
     # seeded random batches: block length, head grouping, head dimension,
     # vocabulary, prompt and generation lengths, block indices (partial last
-    # blocks, empty suffixes), row order with unused rows and padding slack
+    # blocks, empty suffixes), row order with unused rows and padding slack;
+    # the small ones leave CUs idle, so seeds 1-3, 11, 15, 19 and 20 (MHA)
+    # run split-KV plans
     torch, bs, bstep = lazy()
     g_ = np.random.default_rng(9000 + seed)
     L = int(g_.choice([8, 16, 32, 64]))
